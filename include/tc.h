@@ -1,0 +1,191 @@
+/*
+ * tc.h - tensor-group collectives and the fused elastic-averaging SGD step
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The method is that of MXNET-MPI (Mamidala, Kollias, Ward, Artico, arXiv
+ * 1801.03855): a worker's per-layer tensors are handled as one object, K
+ * per-worker copies of it are summed or averaged, and the averaging is fused
+ * with the elastic-averaging SGD update.  Here the K workers' copies are K
+ * buffers resident in one GPU's memory.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Plain C ABI.  Pointers marked "device" point to GPU memory of the device
+ *   that was current when the group was created; arrays of such pointers
+ *   (x[], grad[], in[], flat[], tensors[]) are HOST arrays that the call
+ *   reads before it returns.
+ * - All data buffers are owned by the caller.  The library owns only the
+ *   descriptors it returns (tc_group, tc_tensorlist) and their device tables.
+ * - `stream` is a hipStream_t passed as void*; NULL is the null stream.
+ *   Every data operation is enqueued asynchronously on it, and nothing waits
+ *   for it to finish; faults during execution surface at the caller's next
+ *   synchronisation.
+ * - Return value of the data operations: TC_OK, or a negative tc_status.
+ *   On error nothing has been enqueued, except TC_EHIP from a failed launch;
+ *   tc_last_error() then describes the error (thread-local, valid until the
+ *   next call on the same thread).
+ * - A flat buffer of a group holds N = sum(sizes) elements, densely
+ *   concatenated in tensor order with no padding.  Buffers need only the
+ *   alignment of their element type; 16-byte aligned buffers take the
+ *   vectorised path.
+ * - Binary32 arithmetic, round to nearest even, no flush of subnormals.
+ *   bfloat16 inputs are widened exactly to binary32.
+ */
+#ifndef TC_H
+#define TC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tc_group tc_group;           /* opaque, library-owned */
+typedef struct tc_tensorlist tc_tensorlist; /* opaque, library-owned */
+
+typedef enum { TC_SUM = 0, TC_AVG = 1 } tc_op;
+typedef enum { TC_F32 = 0, TC_BF16 = 1 } tc_dtype;
+typedef enum {
+    TC_OK = 0,
+    TC_EINVAL = -1,       /* bad argument; nothing enqueued */
+    TC_ENOMEM = -2,       /* a device or host allocation failed */
+    TC_EHIP = -3,         /* a HIP call or kernel launch failed */
+    TC_EUNSUPPORTED = -4  /* valid request the library does not implement */
+} tc_status;
+
+/* Largest number of worker copies K accepted by any entry point. */
+#define TC_MAX_K 64
+
+/* Thread-local description of the last error on this thread ("" if none). */
+const char* tc_last_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int32_t tc_version(void);
+
+/* ------------------------------------------------------------------------
+ * Tensor group descriptor.
+ *
+ * A group is the ordered list of a model's layer tensors (one key per layer,
+ * keys in layer order: Sec. 3.2 of the paper) treated as one flat object
+ * (the "tensor" of Sec. 6.1).  Tensor t occupies flat positions
+ * [offsets[t], offsets[t+1]), offsets[0] = 0, offsets[t+1] = offsets[t] +
+ * sizes[t].
+ *
+ * tc_group_create: sizes is a host array of n >= 1 element counts, each
+ * >= 0 (zero-size tensors are allowed); it is copied.  Builds the offset
+ * table and the per-chunk segment table used by tc_pack / tc_unpack, and
+ * copies both to the current device (synchronously; this is set-up, not
+ * part of a step).  Returns NULL on error (n < 1, a negative size, a total
+ * that overflows int64, allocation failure, no device); see tc_last_error.
+ * ---------------------------------------------------------------------- */
+tc_group* tc_group_create(const int64_t* sizes, int32_t n);
+
+/* Frees the group and its device tables.  NULL-safe.  Must not be called
+ * while work that uses the group is still pending on a stream. */
+void tc_group_destroy(tc_group* g);
+
+/* N = sum of the sizes, or -1 if g is NULL. */
+int64_t tc_group_numel(const tc_group* g);
+
+/* Number of tensors n, or -1 if g is NULL. */
+int32_t tc_group_ntensors(const tc_group* g);
+
+/* Copies the n+1 offsets into the host array out.  TC_EINVAL on NULL. */
+int32_t tc_group_offsets(const tc_group* g, int64_t* out);
+
+/* ------------------------------------------------------------------------
+ * Tensor list: K copies of a group held as separate per-layer tensors (the
+ * paper's "tensorlist", Sec. 3.2: for every key one tensor per worker).
+ *
+ * ptrs is a host array of K*n device pointers, copy-major: ptrs[k*n + t] is
+ * tensor t of copy k and holds sizes[t] elements of `dtype`, contiguous,
+ * aligned to the element size.  A zero-size tensor's pointer may be NULL.
+ * The pointer table is copied to the device once (synchronously); the
+ * tensors themselves stay owned by the caller and must outlive the list.
+ * Returns NULL on error (K outside [1, TC_MAX_K], a NULL pointer for a
+ * non-empty tensor, misalignment, bad dtype, allocation failure).
+ * ---------------------------------------------------------------------- */
+tc_tensorlist* tc_tensorlist_create(const tc_group* g, int32_t K,
+                                    const void* const* ptrs, int32_t dtype);
+
+/* Frees the list's device table.  NULL-safe.  The group must outlive it. */
+void tc_tensorlist_destroy(tc_tensorlist* tl);
+
+/* ------------------------------------------------------------------------
+ * tc_pack: gather every copy's tensors into its flat buffer,
+ *   flat[k][offsets[t] + e] = tensor(k, t)[e]      for all k < K, t, e,
+ * bit for bit (push collects the key list, Sec. 3.2).  flat is a host array
+ * of K device pointers, each to N elements of the list's dtype.  One launch
+ * for all K copies and all n tensors.  Flat buffers must not overlap the
+ * tensors or each other.
+ * ---------------------------------------------------------------------- */
+int32_t tc_pack(const tc_tensorlist* tl, void* const* flat, void* stream);
+
+/* ------------------------------------------------------------------------
+ * tc_unpack: scatter every copy's flat buffer back to its tensors,
+ *   tensor(k, t)[e] = flat[k][offsets[t] + e],
+ * bit for bit (pull copies the value to every tensor of the list,
+ * Sec. 3.2).  Same layout and rules as tc_pack.
+ * ---------------------------------------------------------------------- */
+int32_t tc_unpack(const tc_tensorlist* tl, const void* const* flat, void* stream);
+
+/* ------------------------------------------------------------------------
+ * tc_reduce: K-way reduction of flat copies (the tensor reduction of
+ * Sec. 6.3 and Sec. 7.3; push sums the tensors of a key, Sec. 3.2; the
+ * synchronous SGD rescale by 1/mini_batch_size makes it an average, Sec. 5):
+ *   out[j] = in_0[j] + ... + in_{K-1}[j]          (TC_SUM)
+ *   out[j] = (in_0[j] + ... + in_{K-1}[j]) / K    (TC_AVG)
+ * for j < N.  in is a host array of K device pointers to N binary32 values;
+ * out is a device pointer to N binary32 values.  The K terms are added as a
+ * pairwise tree (adjacent pairs, level by level; an odd last term is carried
+ * up), and AVG divides the sum by K with one correctly rounded division; so
+ * the AVG of K identical copies returns the copy exactly for power-of-two K.
+ * out may be identical to one of the inputs (in place); partial overlaps are
+ * undefined.  K in [1, TC_MAX_K].
+ * ---------------------------------------------------------------------- */
+int32_t tc_reduce(const tc_group* g, int32_t K, const float* const* in,
+                  float* out, int32_t op, void* stream);
+
+/* As tc_reduce, with inputs of type in_dtype (TC_F32 or TC_BF16); the sum
+ * is accumulated and returned in binary32. */
+int32_t tc_reduce_ex(const tc_group* g, int32_t K, const void* const* in,
+                     int32_t in_dtype, float* out, int32_t op, void* stream);
+
+/* ------------------------------------------------------------------------
+ * easgd_step: one synchronous elastic-averaging SGD step over K workers,
+ * fused with the K-way reduction of the center's elastic term, in place.
+ * For every j < N, with c = x_c[j] and x_i = x[i][j] read before any write:
+ *
+ *   d_i       = x_i - c
+ *   x[i][j]   = x_i - eta * (grad_i[j] + rho * d_i)
+ *   x_c[j]    = c + (eta*rho) * (d_0 + ... + d_{K-1})
+ *
+ * The worker line is the client's elastic move (Sec. 2.2, Eq. 3, with
+ * alpha = eta*rho) followed by the SGD move -eta*g (Sec. 2.1, Eq. 1); the
+ * center line is the server's elastic move (Sec. 2.2, Eq. 2) summed over
+ * the K workers.  Arithmetic: d_i = x_i - c; t = fma(rho, d_i, g_i);
+ * x_i' = fma(-eta, t, x_i); the d_i are summed by the same pairwise tree as
+ * tc_reduce; x_c' = fma(eta*rho, sum, c), with eta*rho rounded once to
+ * binary32.
+ *
+ * x: host array of K device pointers to N binary32 worker values (in/out),
+ * pairwise distinct.  grad: host array of K device pointers to N binary32
+ * gradients (read only; may alias each other, not x or x_c).  x_c: device
+ * pointer to N binary32 center values (in/out), distinct from all others.
+ * eta, rho: finite.  TC_EINVAL on K outside [1, TC_MAX_K], NULL pointers
+ * with N > 0, non-finite eta or rho.
+ * ---------------------------------------------------------------------- */
+int32_t easgd_step(const tc_group* g, int32_t K, float* const* x,
+                   const float* const* grad, float* x_c, float eta, float rho,
+                   void* stream);
+
+/* As easgd_step, with gradients of type g_dtype (TC_F32 or TC_BF16). */
+int32_t easgd_step_ex(const tc_group* g, int32_t K, float* const* x,
+                      const void* const* grad, int32_t g_dtype, float* x_c,
+                      float eta, float rho, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TC_H */

@@ -1,0 +1,221 @@
+"""Tensor-group collectives and the fused elastic-averaging SGD step on
+AMD MI355X (gfx950).
+
+A thin ctypes binding of the C ABI declared in ``include/tc.h``: every
+function here marshals torch tensors into device pointers, sizes and the
+current HIP stream, and calls the library of the same name.  All arithmetic
+runs in the library's HIP kernels; there is no CPU or PyTorch fallback, and
+loading fails loudly when the library has not been built.
+
+    g = Group(sizes)                        # tc_group_create
+    tl = TensorList(g, [[t00, t01, ...], [t10, ...]])   # tc_tensorlist_create
+    pack(tl, flats); unpack(tl, flats)      # tc_pack / tc_unpack
+    reduce(g, ins, out, "avg")              # tc_reduce / tc_reduce_ex
+    easgd_step(g, xs, gs, xc, eta, rho)     # easgd_step / easgd_step_ex
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+from .build import LIBRARY
+
+TC_SUM, TC_AVG = 0, 1
+TC_F32, TC_BF16 = 0, 1
+TC_OK, TC_EINVAL, TC_ENOMEM, TC_EHIP, TC_EUNSUPPORTED = 0, -1, -2, -3, -4
+TC_MAX_K = 64
+
+_OPS = {"sum": TC_SUM, "avg": TC_AVG, TC_SUM: TC_SUM, TC_AVG: TC_AVG}
+_DTYPES = {torch.float32: TC_F32, torch.bfloat16: TC_BF16}
+
+
+class TCError(RuntimeError):
+    """A C-ABI call returned an error status."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(f"[{status}] {message}")
+        self.status = status
+
+
+_VP = ctypes.c_void_p
+_VPP = ctypes.POINTER(ctypes.c_void_p)
+_lib = None
+
+
+def lib(path: str = LIBRARY) -> ctypes.CDLL:
+    """The loaded HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP library {path} is not built; run __graft_entry__.build() "
+                           f"or python -m paper_1801_03855_amd.build")
+    L = ctypes.CDLL(path)
+    i32, i64, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    sig = {
+        "tc_last_error": (ctypes.c_char_p, []),
+        "tc_version": (i32, []),
+        "tc_group_create": (_VP, [ctypes.POINTER(i64), i32]),
+        "tc_group_destroy": (None, [_VP]),
+        "tc_group_numel": (i64, [_VP]),
+        "tc_group_ntensors": (i32, [_VP]),
+        "tc_group_offsets": (i32, [_VP, ctypes.POINTER(i64)]),
+        "tc_tensorlist_create": (_VP, [_VP, i32, _VPP, i32]),
+        "tc_tensorlist_destroy": (None, [_VP]),
+        "tc_pack": (i32, [_VP, _VPP, _VP]),
+        "tc_unpack": (i32, [_VP, _VPP, _VP]),
+        "tc_reduce": (i32, [_VP, i32, _VPP, _VP, i32, _VP]),
+        "tc_reduce_ex": (i32, [_VP, i32, _VPP, i32, _VP, i32, _VP]),
+        "easgd_step": (i32, [_VP, i32, _VPP, _VPP, _VP, f32, f32, _VP]),
+        "easgd_step_ex": (i32, [_VP, i32, _VPP, _VPP, i32, _VP, f32, f32, _VP]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def last_error() -> str:
+    return lib().tc_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != TC_OK:
+        raise TCError(status, last_error())
+
+
+def _ptr_array(ptrs: Sequence[Optional[int]]):
+    arr = (ctypes.c_void_p * max(1, len(ptrs)))()
+    for i, p in enumerate(ptrs):
+        arr[i] = p if p else None
+    return arr
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev_ptr(t: torch.Tensor, n: int, dtypes=(torch.float32,), what: str = "tensor") -> int:
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a GPU tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{what} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous() or t.numel() < n:
+        raise ValueError(f"{what} must be contiguous with at least {n} elements (has {t.numel()})")
+    return t.data_ptr()
+
+
+class Group:
+    """A tensor group: n layer sizes, one flat index space of N elements."""
+
+    def __init__(self, sizes: Sequence[int]):
+        arr = (ctypes.c_int64 * len(sizes))(*[int(s) for s in sizes])
+        h = lib().tc_group_create(arr, len(sizes))
+        if not h:
+            raise TCError(TC_EINVAL, last_error())
+        self._h = h
+        self.sizes = [int(s) for s in sizes]
+        self.n = lib().tc_group_ntensors(h)
+        self.numel = lib().tc_group_numel(h)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def offsets(self):
+        out = (ctypes.c_int64 * (self.n + 1))()
+        _check(lib().tc_group_offsets(self._h, out))
+        return list(out)
+
+    def __del__(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h and _lib is not None:
+            _lib.tc_group_destroy(h)
+
+
+class TensorList:
+    """K copies of a group as separate tensors: tensors[k][t] is tensor t of
+    copy k (a contiguous GPU tensor of sizes[t] elements)."""
+
+    def __init__(self, group: Group, tensors: Sequence[Sequence[torch.Tensor]]):
+        K = len(tensors)
+        dt = None
+        ptrs = []
+        for k, copy in enumerate(tensors):
+            if len(copy) != group.n:
+                raise ValueError(f"copy {k} has {len(copy)} tensors, the group has {group.n}")
+            for t, (x, s) in enumerate(zip(copy, group.sizes)):
+                dt = dt or x.dtype
+                if x.dtype != dt or x.dtype not in _DTYPES:
+                    raise TypeError(f"tensor ({k},{t}) has dtype {x.dtype}")
+                if x.numel() != s:
+                    raise ValueError(f"tensor ({k},{t}) has {x.numel()} elements, expected {s}")
+                ptrs.append(_dev_ptr(x, s, (dt,), f"tensor ({k},{t})") if s else 0)
+        self.group, self.K, self.dtype = group, K, dt
+        self._keep = [list(c) for c in tensors]
+        h = lib().tc_tensorlist_create(group.handle, K, _ptr_array(ptrs), _DTYPES[dt])
+        if not h:
+            raise TCError(TC_EINVAL, last_error())
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    def __del__(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h and _lib is not None:
+            _lib.tc_tensorlist_destroy(h)
+
+
+def _flat_ptrs(tl: TensorList, flats: Sequence[torch.Tensor]):
+    if len(flats) != tl.K:
+        raise ValueError(f"need {tl.K} flat buffers, got {len(flats)}")
+    n = tl.group.numel
+    return _ptr_array([_dev_ptr(f, n, (tl.dtype,), f"flat[{k}]") for k, f in enumerate(flats)])
+
+
+def pack(tl: TensorList, flats: Sequence[torch.Tensor], stream=None) -> None:
+    """flats[k][offsets[t] + e] = tensors[k][t][e] (tc_pack)."""
+    _check(lib().tc_pack(tl.handle, _flat_ptrs(tl, flats), _stream(stream)))
+
+
+def unpack(tl: TensorList, flats: Sequence[torch.Tensor], stream=None) -> None:
+    """tensors[k][t][e] = flats[k][offsets[t] + e] (tc_unpack)."""
+    _check(lib().tc_unpack(tl.handle, _flat_ptrs(tl, flats), _stream(stream)))
+
+
+def reduce(group: Group, ins: Sequence[torch.Tensor], out: torch.Tensor, op="avg", stream=None) -> None:
+    """out = sum (or average) of the K flat copies ins (tc_reduce_ex)."""
+    n = group.numel
+    dt = ins[0].dtype
+    if dt not in _DTYPES:
+        raise TypeError(f"inputs have dtype {dt}")
+    p = _ptr_array([_dev_ptr(t, n, (dt,), f"in[{i}]") for i, t in enumerate(ins)])
+    _check(lib().tc_reduce_ex(group.handle, len(ins), p, _DTYPES[dt],
+                              _dev_ptr(out, n, (torch.float32,), "out"), _OPS[op], _stream(stream)))
+
+
+def easgd_step(group: Group, xs: Sequence[torch.Tensor], gs: Sequence[torch.Tensor], xc: torch.Tensor,
+               eta: float, rho: float, stream=None) -> None:
+    """One fused elastic-averaging SGD step, in place on xs and xc
+    (easgd_step_ex)."""
+    n = group.numel
+    if len(xs) != len(gs):
+        raise ValueError("need one gradient per worker")
+    gdt = gs[0].dtype
+    if gdt not in _DTYPES:
+        raise TypeError(f"gradients have dtype {gdt}")
+    xp = _ptr_array([_dev_ptr(t, n, (torch.float32,), f"x[{i}]") for i, t in enumerate(xs)])
+    gp = _ptr_array([_dev_ptr(t, n, (gdt,), f"grad[{i}]") for i, t in enumerate(gs)])
+    _check(lib().easgd_step_ex(group.handle, len(xs), xp, gp, _DTYPES[gdt],
+                               _dev_ptr(xc, n, (torch.float32,), "x_c"), float(eta), float(rho),
+                               _stream(stream)))

@@ -1,0 +1,63 @@
+"""Compiles the HIP library (``libtc_amd.so``) for gfx950 with hipcc.
+
+``python -m paper_1801_03855_amd.build`` or ``build()`` from Python.  Extra
+``-D`` definitions (kernel tunables) and a different output path may be
+given, which is how variant builds for tuning are made without touching the
+sources.
+"""
+
+from __future__ import annotations
+
+import glob
+import os
+import subprocess
+import sys
+from typing import Sequence
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIBRARY = os.path.join(PKG, "libtc_amd.so")
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+FLAGS = [
+    "--offload-arch=gfx950",
+    "-O3",
+    "-std=c++17",
+    "-fPIC",
+    "-shared",
+    "-fvisibility=hidden",
+    # binary32 arithmetic exactly as written: fused multiply-adds only where
+    # the source calls fma
+    "-ffp-contract=off",
+    # no packed-FP32 instructions
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall",
+]
+
+
+def sources() -> list:
+    return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+
+
+def build(output: str = LIBRARY, defines: Sequence[str] = (), verbose: bool = False) -> str:
+    cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines], "-I", INCLUDE, "-I", CSRC,
+           "-o", output + ".tmp", *sources()]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(output + ".tmp", output)
+    return output
+
+
+if __name__ == "__main__":
+    out = LIBRARY
+    defs = []
+    for arg in sys.argv[1:]:
+        if arg.startswith("-D"):
+            defs.append(arg[2:])
+        elif arg.startswith("-o"):
+            out = arg[2:]
+    print(build(out, defs, verbose=True))

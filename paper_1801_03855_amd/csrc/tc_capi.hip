@@ -1,0 +1,275 @@
+// C entry points: argument validation, descriptors, dispatch to launchers.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "tc_internal.h"
+
+namespace tc {
+
+static thread_local std::string t_error;
+
+void set_error(const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_error = buf;
+}
+
+void clear_error() { t_error.clear(); }
+
+namespace {
+
+int32_t fail(int32_t code, const char* what) {
+    set_error("%s", what);
+    return code;
+}
+
+int32_t hip_fail(hipError_t e, const char* where) {
+    set_error("%s: %s", where, hipGetErrorString(e));
+    return TC_EHIP;
+}
+
+int elem_size(int32_t dtype) { return dtype == TC_BF16 ? 2 : dtype == TC_F32 ? 4 : 0; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+// [p, p + bytes) and [q, q + bytes2) share a byte.
+bool overlap(const void* p, int64_t bytes, const void* q, int64_t bytes2) {
+    auto a = reinterpret_cast<uintptr_t>(p), b = reinterpret_cast<uintptr_t>(q);
+    return a < b + static_cast<uintptr_t>(bytes2) && b < a + static_cast<uintptr_t>(bytes);
+}
+
+// The group's device must be the current one.
+int32_t check_device(const tc_group* g) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != g->device) {
+        set_error("the group lives on device %d but device %d is current", g->device, dev);
+        return TC_EINVAL;
+    }
+    return TC_OK;
+}
+
+}  // namespace
+}  // namespace tc
+
+using namespace tc;
+
+TC_API const char* tc_last_error(void) { return t_error.c_str(); }
+
+TC_API int32_t tc_version(void) { return 100; }
+
+// ---------------------------------------------------------------- groups
+
+TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
+    clear_error();
+    if (n < 1) { set_error("n must be >= 1 (got %d)", n); return nullptr; }
+    if (!sizes) { set_error("sizes is NULL"); return nullptr; }
+    auto* g = new (std::nothrow) tc_group();
+    if (!g) { set_error("out of host memory"); return nullptr; }
+    g->n = n;
+    g->sizes.assign(sizes, sizes + n);
+    g->offsets.resize(static_cast<size_t>(n) + 1);
+    g->offsets[0] = 0;
+    for (int32_t t = 0; t < n; ++t) {
+        if (sizes[t] < 0) { set_error("sizes[%d] = %lld is negative", t, (long long)sizes[t]); delete g; return nullptr; }
+        if (sizes[t] > INT64_MAX / 8 - g->offsets[t]) { set_error("group too large"); delete g; return nullptr; }
+        g->offsets[t + 1] = g->offsets[t] + sizes[t];
+    }
+    g->N = g->offsets[n];
+    g->nchunks = (g->N + kChunk - 1) / kChunk;
+    if (g->nchunks > INT32_MAX / 2) { set_error("group too large"); delete g; return nullptr; }
+    // chunk_first[b]: the tensor holding flat position b*kChunk, i.e. the
+    // last tensor whose offset is <= that position (zero-size tensors at the
+    // same offset come before the one that holds it).  The final entry is
+    // the tensor holding position N-1.
+    g->chunk_first.resize(static_cast<size_t>(g->nchunks) + 1);
+    auto tensor_at = [&](int64_t j) {
+        auto it = std::upper_bound(g->offsets.begin(), g->offsets.begin() + n, j);
+        return static_cast<int32_t>(it - g->offsets.begin()) - 1;
+    };
+    for (int64_t b = 0; b < g->nchunks; ++b) g->chunk_first[b] = tensor_at(b * kChunk);
+    g->chunk_first[g->nchunks] = g->N > 0 ? tensor_at(g->N - 1) : 0;
+
+    hipError_t e = hipGetDevice(&g->device);
+    if (e != hipSuccess) { hip_fail(e, "hipGetDevice"); delete g; return nullptr; }
+    size_t ob = g->offsets.size() * sizeof(int64_t), cb = g->chunk_first.size() * sizeof(int32_t);
+    if ((e = hipMalloc(&g->d_offsets, ob)) != hipSuccess ||
+        (e = hipMalloc(&g->d_chunk_first, cb)) != hipSuccess) {
+        hip_fail(e, "hipMalloc (group tables)");
+        tc_group_destroy(g);
+        return nullptr;
+    }
+    if ((e = hipMemcpy(g->d_offsets, g->offsets.data(), ob, hipMemcpyHostToDevice)) != hipSuccess ||
+        (e = hipMemcpy(g->d_chunk_first, g->chunk_first.data(), cb, hipMemcpyHostToDevice)) != hipSuccess) {
+        hip_fail(e, "hipMemcpy (group tables)");
+        tc_group_destroy(g);
+        return nullptr;
+    }
+    return g;
+}
+
+TC_API void tc_group_destroy(tc_group* g) {
+    if (!g) return;
+    if (g->d_offsets) (void)hipFree(g->d_offsets);
+    if (g->d_chunk_first) (void)hipFree(g->d_chunk_first);
+    delete g;
+}
+
+TC_API int64_t tc_group_numel(const tc_group* g) { return g ? g->N : -1; }
+
+TC_API int32_t tc_group_ntensors(const tc_group* g) { return g ? g->n : -1; }
+
+TC_API int32_t tc_group_offsets(const tc_group* g, int64_t* out) {
+    clear_error();
+    if (!g || !out) return fail(TC_EINVAL, "tc_group_offsets: NULL argument");
+    std::memcpy(out, g->offsets.data(), g->offsets.size() * sizeof(int64_t));
+    return TC_OK;
+}
+
+// ----------------------------------------------------------- tensor lists
+
+TC_API tc_tensorlist* tc_tensorlist_create(const tc_group* g, int32_t K, const void* const* ptrs,
+                                           int32_t dtype) {
+    clear_error();
+    if (!g || !ptrs) { set_error("tc_tensorlist_create: NULL argument"); return nullptr; }
+    if (K < 1 || K > TC_MAX_K) { set_error("K = %d outside [1, %d]", K, TC_MAX_K); return nullptr; }
+    const int es = elem_size(dtype);
+    if (!es) { set_error("unknown dtype %d", dtype); return nullptr; }
+    if (check_device(g) != TC_OK) return nullptr;
+    for (int32_t k = 0; k < K; ++k)
+        for (int32_t t = 0; t < g->n; ++t) {
+            const void* p = ptrs[static_cast<int64_t>(k) * g->n + t];
+            if (g->sizes[t] == 0) continue;
+            if (!p) { set_error("tensor %d of copy %d is NULL", t, k); return nullptr; }
+            if (!aligned(p, es)) { set_error("tensor %d of copy %d is not %d-byte aligned", t, k, es); return nullptr; }
+        }
+    auto* tl = new (std::nothrow) tc_tensorlist();
+    if (!tl) { set_error("out of host memory"); return nullptr; }
+    tl->g = g;
+    tl->K = K;
+    tl->dtype = dtype;
+    tl->elem = es;
+    tl->ptrs.assign(ptrs, ptrs + static_cast<int64_t>(K) * g->n);
+    const size_t bytes = tl->ptrs.size() * sizeof(void*);
+    hipError_t e = hipMalloc(&tl->d_ptrs, bytes);
+    if (e != hipSuccess) { hip_fail(e, "hipMalloc (pointer table)"); delete tl; return nullptr; }
+    e = hipMemcpy(tl->d_ptrs, tl->ptrs.data(), bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) { hip_fail(e, "hipMemcpy (pointer table)"); tc_tensorlist_destroy(tl); return nullptr; }
+    return tl;
+}
+
+TC_API void tc_tensorlist_destroy(tc_tensorlist* tl) {
+    if (!tl) return;
+    if (tl->d_ptrs) (void)hipFree(tl->d_ptrs);
+    delete tl;
+}
+
+// ------------------------------------------------------------ pack/unpack
+
+static int32_t pack_common(const tc_tensorlist* tl, void* const* flat, bool unpack, void* stream) {
+    clear_error();
+    if (!tl || !flat) return fail(TC_EINVAL, "NULL argument");
+    const tc_group* g = tl->g;
+    if (int32_t r = check_device(g)) return r;
+    if (g->N == 0) return TC_OK;
+    bool flat_aligned = true;
+    const int64_t bytes = g->N * tl->elem;
+    for (int32_t k = 0; k < tl->K; ++k) {
+        if (!flat[k]) { set_error("flat[%d] is NULL", k); return TC_EINVAL; }
+        if (!aligned(flat[k], tl->elem)) { set_error("flat[%d] is not element-aligned", k); return TC_EINVAL; }
+        flat_aligned = flat_aligned && aligned(flat[k], 16);
+        for (int32_t q = 0; q < k; ++q)
+            if (overlap(flat[k], bytes, flat[q], bytes)) { set_error("flat[%d] overlaps flat[%d]", k, q); return TC_EINVAL; }
+    }
+    hipError_t e = launch_pack(tl, flat, unpack, flat_aligned, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, unpack ? "tc_unpack launch" : "tc_pack launch");
+    return TC_OK;
+}
+
+TC_API int32_t tc_pack(const tc_tensorlist* tl, void* const* flat, void* stream) {
+    return pack_common(tl, flat, false, stream);
+}
+
+TC_API int32_t tc_unpack(const tc_tensorlist* tl, const void* const* flat, void* stream) {
+    return pack_common(tl, const_cast<void* const*>(flat), true, stream);
+}
+
+// ----------------------------------------------------------------- reduce
+
+TC_API int32_t tc_reduce_ex(const tc_group* g, int32_t K, const void* const* in, int32_t in_dtype,
+                            float* out, int32_t op, void* stream) {
+    clear_error();
+    if (!g) return fail(TC_EINVAL, "group is NULL");
+    if (K < 1 || K > TC_MAX_K) { set_error("K = %d outside [1, %d]", K, TC_MAX_K); return TC_EINVAL; }
+    if (op != TC_SUM && op != TC_AVG) { set_error("unknown op %d", op); return TC_EINVAL; }
+    const int es = elem_size(in_dtype);
+    if (!es) { set_error("unknown dtype %d", in_dtype); return TC_EINVAL; }
+    if (int32_t r = check_device(g)) return r;
+    if (g->N == 0) return TC_OK;
+    if (!in || !out) return fail(TC_EINVAL, "NULL buffer");
+    bool vec = aligned(out, 16);
+    if (!aligned(out, 4)) return fail(TC_EINVAL, "out is not 4-byte aligned");
+    for (int32_t i = 0; i < K; ++i) {
+        if (!in[i]) { set_error("in[%d] is NULL", i); return TC_EINVAL; }
+        if (!aligned(in[i], es)) { set_error("in[%d] is not element-aligned", i); return TC_EINVAL; }
+        vec = vec && aligned(in[i], es == 4 ? 16 : 8);
+        // in place is allowed only as exact identity with an input
+        if (in[i] != out && overlap(in[i], g->N * es, out, g->N * 4)) {
+            set_error("out partially overlaps in[%d]", i);
+            return TC_EINVAL;
+        }
+    }
+    hipError_t e = launch_reduce(K, in, in_dtype, out, op, g->N, vec, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "tc_reduce launch");
+    return TC_OK;
+}
+
+TC_API int32_t tc_reduce(const tc_group* g, int32_t K, const float* const* in, float* out, int32_t op,
+                         void* stream) {
+    return tc_reduce_ex(g, K, reinterpret_cast<const void* const*>(in), TC_F32, out, op, stream);
+}
+
+// ------------------------------------------------------------------ easgd
+
+TC_API int32_t easgd_step_ex(const tc_group* g, int32_t K, float* const* x, const void* const* grad,
+                             int32_t g_dtype, float* x_c, float eta, float rho, void* stream) {
+    clear_error();
+    if (!g) return fail(TC_EINVAL, "group is NULL");
+    if (K < 1 || K > TC_MAX_K) { set_error("K = %d outside [1, %d]", K, TC_MAX_K); return TC_EINVAL; }
+    const int es = elem_size(g_dtype);
+    if (!es) { set_error("unknown dtype %d", g_dtype); return TC_EINVAL; }
+    if (!std::isfinite(eta) || !std::isfinite(rho)) return fail(TC_EINVAL, "eta and rho must be finite");
+    if (int32_t r = check_device(g)) return r;
+    if (g->N == 0) return TC_OK;
+    if (!x || !grad || !x_c) return fail(TC_EINVAL, "NULL buffer");
+    const int64_t xb = g->N * 4, gb = g->N * es;
+    if (!aligned(x_c, 4)) return fail(TC_EINVAL, "x_c is not 4-byte aligned");
+    bool vec = aligned(x_c, 16);
+    for (int32_t i = 0; i < K; ++i) {
+        if (!x[i] || !grad[i]) { set_error("x[%d] or grad[%d] is NULL", i, i); return TC_EINVAL; }
+        if (!aligned(x[i], 4) || !aligned(grad[i], es)) { set_error("x[%d] or grad[%d] misaligned", i, i); return TC_EINVAL; }
+        vec = vec && aligned(x[i], 16) && aligned(grad[i], es == 4 ? 16 : 8);
+        if (overlap(x[i], xb, x_c, xb)) { set_error("x[%d] overlaps x_c", i); return TC_EINVAL; }
+        if (overlap(grad[i], gb, x_c, xb)) { set_error("grad[%d] overlaps x_c", i); return TC_EINVAL; }
+        for (int32_t q = 0; q < K; ++q) {
+            if (q < i && overlap(x[i], xb, x[q], xb)) { set_error("x[%d] overlaps x[%d]", i, q); return TC_EINVAL; }
+            if (overlap(grad[q], gb, x[i], xb)) { set_error("grad[%d] overlaps x[%d]", q, i); return TC_EINVAL; }
+        }
+    }
+    hipError_t e = launch_easgd(K, x, grad, g_dtype, x_c, eta, rho, g->N, vec, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "easgd_step launch");
+    return TC_OK;
+}
+
+TC_API int32_t easgd_step(const tc_group* g, int32_t K, float* const* x, const float* const* grad, float* x_c,
+                          float eta, float rho, void* stream) {
+    return easgd_step_ex(g, K, x, reinterpret_cast<const void* const*>(grad), TC_F32, x_c, eta, rho, stream);
+}

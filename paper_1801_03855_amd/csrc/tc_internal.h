@@ -1,0 +1,64 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <vector>
+
+#include "tc.h"
+
+#define TC_API extern "C" __attribute__((visibility("default")))
+
+namespace tc {
+
+// Elements per pack/unpack chunk; one workgroup gathers or scatters one
+// chunk of one copy.  A multiple of every vector width used (4 and 8).
+constexpr int64_t kChunk = 4096;
+
+// Segments (tensors overlapping one chunk) whose offsets and pointers a
+// workgroup stages in LDS; chunks touching more tensors search the global
+// tables instead.
+constexpr int kMaxStage = 1024;
+
+// Records a printf-style message as this thread's last error.
+void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+void clear_error();
+
+// Launchers, defined next to their kernels.  Arguments are validated by the
+// caller; these only pick a kernel and enqueue it on `stream`.
+hipError_t launch_reduce(int K, const void* const* in, int in_dtype, float* out, int op,
+                         int64_t n, bool vector_ok, hipStream_t stream);
+hipError_t launch_easgd(int K, float* const* x, const void* const* g, int g_dtype, float* xc,
+                        float eta, float rho, int64_t n, bool vector_ok, hipStream_t stream);
+
+struct PackArgs;  // defined in tc_pack.hip
+hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, bool flat_aligned,
+                       hipStream_t stream);
+
+}  // namespace tc
+
+// Group descriptor: host copies of sizes and offsets, and device copies of
+// the offset table and of the per-chunk first-segment table.
+struct tc_group {
+    int32_t n = 0;
+    int64_t N = 0;
+    int device = 0;
+    std::vector<int64_t> sizes;
+    std::vector<int64_t> offsets;      // n + 1
+    int64_t nchunks = 0;               // ceil(N / kChunk)
+    std::vector<int32_t> chunk_first;  // nchunks + 1
+    int64_t* d_offsets = nullptr;
+    int32_t* d_chunk_first = nullptr;
+};
+
+// K copies of a group held as separate tensors: device table of K*n
+// pointers, copy-major.
+struct tc_tensorlist {
+    const tc_group* g = nullptr;
+    int32_t K = 0;
+    int32_t dtype = TC_F32;
+    int32_t elem = 4;
+    std::vector<const void*> ptrs;
+    void** d_ptrs = nullptr;
+};
