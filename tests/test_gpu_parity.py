@@ -492,6 +492,10 @@ def test_argument_errors():
     assert L.easgd_step(g.handle, 3, xp, gp, xc.data_ptr(), 0.1, 0.5, s) == tc.TC_OK
     with pytest.raises(tc.TCError):
         tc.Group([3, -1])
-    with pytest.raises(tc.TCError):
-        tc.TensorList(g, [])  # K = 0
+    arr = tc._ptr_array([a[0].data_ptr()])
+    assert not L.tc_tensorlist_create(g.handle, 0, arr, tc.TC_F32)   # K = 0
+    assert not L.tc_tensorlist_create(g.handle, 1, arr, 9)           # unknown dtype
+    null = tc._ptr_array([0])
+    assert not L.tc_tensorlist_create(g.handle, 1, null, tc.TC_F32)  # NULL non-empty tensor
+    assert "NULL" in tc.last_error()
     torch.cuda.synchronize()
