@@ -6,9 +6,10 @@
 //
 // Mapping: one lane owns one 16-byte slot of every stream (4 binary32
 // values; 4 bfloat16 gradients are 8 bytes), so each wave instruction moves
-// 1 KiB (512 B for bfloat16) of contiguous memory per buffer.  A lane issues
-// the loads of all 2K+1 streams of its slot before any arithmetic, keeping
-// (2K+1) x 16 B in flight per lane.  Workgroups walk the slots grid-stride.
+// 1 KiB (512 B for bfloat16) of contiguous memory per buffer.  A lane owns
+// two slots (one per half of its workgroup's tile) and issues the loads of
+// all 2K+1 streams of both before any arithmetic.  One workgroup per tile;
+// non-temporal loads and stores, since nothing is re-read.
 // A ragged tail of fewer than 4 elements is handled element by element by
 // the last workgroup; buffers that are not 16-byte aligned take the
 // element-by-element kernel.
@@ -21,8 +22,11 @@
 #ifndef TC_EW_THREADS
 #define TC_EW_THREADS 256
 #endif
+// Workgroups per CU when the grid is capped; 0 launches one workgroup per
+// tile of TC_EW_THREADS * unroll slots (measured fastest on MI355X: the
+// dispatcher then keeps the active window of every stream compact).
 #ifndef TC_EW_BLOCKS_PER_CU
-#define TC_EW_BLOCKS_PER_CU 8
+#define TC_EW_BLOCKS_PER_CU 0
 #endif
 #ifndef TC_NT_LOADS
 #define TC_NT_LOADS 1
@@ -64,29 +68,41 @@ __device__ __forceinline__ void st(T* p, T v) {
 __device__ __forceinline__ float bf16_lo(unsigned int w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(unsigned int w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Value type V is f4 (one 16-byte slot, index = slot) or float (index =
-// element).
+// Value type V is f4 (one 16-byte slot; index = slot) or float (index =
+// element).  Index type I is uint32_t when every buffer is below 4 GiB: the
+// address is then a uniform 64-bit base plus one 32-bit byte offset that all
+// streams share, which the compiler emits as SGPR-base + VGPR-offset loads
+// and stores instead of one 64-bit VGPR address per stream.
+template <typename I>
+__device__ __forceinline__ const char* at(const void* p, I byte_off) {
+    return static_cast<const char*>(p) + byte_off;
+}
+
 template <typename V> struct Mem;
 
 template <> struct Mem<f4> {
-    static __device__ __forceinline__ f4 load(const float* p, int64_t i) {
-        return ld(reinterpret_cast<const f4*>(p) + i);
+    template <typename I> static __device__ __forceinline__ f4 load(const float* p, I i) {
+        return ld(reinterpret_cast<const f4*>(at(p, i * I(16))));
     }
-    static __device__ __forceinline__ f4 load(const uint16_t* p, int64_t i) {
-        u2 w = ld(reinterpret_cast<const u2*>(p) + i);
+    template <typename I> static __device__ __forceinline__ f4 load(const uint16_t* p, I i) {
+        u2 w = ld(reinterpret_cast<const u2*>(at(p, i * I(8))));
         return f4{bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y)};
     }
-    static __device__ __forceinline__ void store(float* p, int64_t i, f4 v) {
-        st(reinterpret_cast<f4*>(p) + i, v);
+    template <typename I> static __device__ __forceinline__ void store(float* p, I i, f4 v) {
+        st(reinterpret_cast<f4*>(const_cast<char*>(at(p, i * I(16)))), v);
     }
 };
 
 template <> struct Mem<float> {
-    static __device__ __forceinline__ float load(const float* p, int64_t i) { return ld(p + i); }
-    static __device__ __forceinline__ float load(const uint16_t* p, int64_t i) {
-        return __uint_as_float(static_cast<unsigned int>(ld(p + i)) << 16);
+    template <typename I> static __device__ __forceinline__ float load(const float* p, I i) {
+        return ld(reinterpret_cast<const float*>(at(p, i * I(4))));
     }
-    static __device__ __forceinline__ void store(float* p, int64_t i, float v) { st(p + i, v); }
+    template <typename I> static __device__ __forceinline__ float load(const uint16_t* p, I i) {
+        return __uint_as_float(static_cast<unsigned int>(ld(reinterpret_cast<const uint16_t*>(at(p, i * I(2))))) << 16);
+    }
+    template <typename I> static __device__ __forceinline__ void store(float* p, I i, float v) {
+        st(reinterpret_cast<float*>(const_cast<char*>(at(p, i * I(4)))), v);
+    }
 };
 
 // ------------------------------------------------------------ arithmetic
@@ -122,20 +138,26 @@ struct ReduceArgs {
     int k_total;  // the number of copies (== K except in the generic kernel)
 };
 
-template <int K, typename T, typename V>
-__device__ __forceinline__ void reduce_slot(const ReduceArgs<K, T>& a, int64_t i) {
-    V v[K];
+// U slots per lane at a time (slot i + u*TC_EW_THREADS), all loads first.
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void reduce_slots(const ReduceArgs<K, T>& a, I i, I du) {
+    V v[U][K];
 #pragma unroll
-    for (int q = 0; q < K; ++q) v[q] = Mem<V>::load(a.in[q], i);
-    V s = Tree<K>::sum(v);
-    if (a.op == TC_AVG) s = s / splat<V>(static_cast<float>(K));
-    Mem<V>::store(a.out, i, s);
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int q = 0; q < K; ++q) v[u][q] = Mem<V>::load(a.in[q], i + I(u) * du);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        V s = Tree<K>::sum(v[u]);
+        if (a.op == TC_AVG) s = s / splat<V>(static_cast<float>(K));
+        Mem<V>::store(a.out, i + I(u) * du, s);
+    }
 }
 
 // Generic K (> kSpecialisedK): trees of 16 zero-padded, then a tree of the
 // at most TC_MAX_K/16 partial sums (zero-padded).
-template <typename T, typename V>
-__device__ __forceinline__ void reduce_slot_generic(const ReduceArgs<TC_MAX_K, T>& a, int64_t i) {
+template <typename T, typename V, typename I>
+__device__ __forceinline__ void reduce_slot_generic(const ReduceArgs<TC_MAX_K, T>& a, I i) {
     constexpr int kParts = TC_MAX_K / kSpecialisedK;
     V part[kParts];
 #pragma unroll
@@ -153,31 +175,10 @@ __device__ __forceinline__ void reduce_slot_generic(const ReduceArgs<TC_MAX_K, T
     Mem<V>::store(a.out, i, s);
 }
 
-template <int K, typename T>
-__device__ __forceinline__ void reduce_any(const ReduceArgs<K, T>& a, int64_t i, f4) {
-    if constexpr (K == TC_MAX_K) reduce_slot_generic<T, f4>(a, i); else reduce_slot<K, T, f4>(a, i);
-}
-template <int K, typename T>
-__device__ __forceinline__ void reduce_any(const ReduceArgs<K, T>& a, int64_t i, float) {
-    if constexpr (K == TC_MAX_K) reduce_slot_generic<T, float>(a, i); else reduce_slot<K, T, float>(a, i);
-}
-
-template <int K, typename T>
-__global__ __launch_bounds__(TC_EW_THREADS) void reduce_vec_kernel(ReduceArgs<K, T> a, int64_t nslot, int64_t n) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * TC_EW_THREADS;
-    for (int64_t s = static_cast<int64_t>(blockIdx.x) * TC_EW_THREADS + threadIdx.x; s < nslot; s += stride)
-        reduce_any<K, T>(a, s, f4{});
-    if (blockIdx.x == gridDim.x - 1) {
-        const int64_t j = 4 * nslot + threadIdx.x;
-        if (j < n) reduce_any<K, T>(a, j, 0.0f);
-    }
-}
-
-template <int K, typename T>
-__global__ __launch_bounds__(TC_EW_THREADS) void reduce_scalar_kernel(ReduceArgs<K, T> a, int64_t n) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * TC_EW_THREADS;
-    for (int64_t j = static_cast<int64_t>(blockIdx.x) * TC_EW_THREADS + threadIdx.x; j < n; j += stride)
-        reduce_any<K, T>(a, j, 0.0f);
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void reduce_any(const ReduceArgs<K, T>& a, I i, I du) {
+    if constexpr (K == TC_MAX_K) reduce_slot_generic<T, V, I>(a, i);
+    else reduce_slots<K, T, U, V, I>(a, i, du);
 }
 
 // ---------------------------------------------------------------- easgd
@@ -191,29 +192,39 @@ struct EasgdArgs {
     int k_total;
 };
 
-template <int K, typename T, typename V>
-__device__ __forceinline__ void easgd_slot(const EasgdArgs<K, T>& a, int64_t i) {
-    const V c = Mem<V>::load(a.xc, i);
-    V x[K], g[K], d[K];
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void easgd_slots(const EasgdArgs<K, T>& a, I i, I du) {
+    V c[U], x[U][K], g[U][K];
 #pragma unroll
-    for (int q = 0; q < K; ++q) {
-        x[q] = Mem<V>::load(a.x[q], i);
-        g[q] = Mem<V>::load(a.g[q], i);
+    for (int u = 0; u < U; ++u) {
+        c[u] = Mem<V>::load(a.xc, i + I(u) * du);
+#pragma unroll
+        for (int q = 0; q < K; ++q) {
+            x[u][q] = Mem<V>::load(a.x[q], i + I(u) * du);
+            g[u][q] = Mem<V>::load(a.g[q], i + I(u) * du);
+        }
     }
-    const V rho = splat<V>(a.rho), neg_eta = splat<V>(-a.eta);
+    const V rho = splat<V>(a.rho), neg_eta = splat<V>(-a.eta), alpha = splat<V>(a.a);
 #pragma unroll
-    for (int q = 0; q < K; ++q) {
-        d[q] = x[q] - c;
-        x[q] = fmav(neg_eta, fmav(rho, d[q], g[q]), x[q]);
+    for (int u = 0; u < U; ++u) {
+        V d[K];
+#pragma unroll
+        for (int q = 0; q < K; ++q) {
+            d[q] = x[u][q] - c[u];
+            x[u][q] = fmav(neg_eta, fmav(rho, d[q], g[u][q]), x[u][q]);
+        }
+        c[u] = fmav(alpha, Tree<K>::sum(d), c[u]);
     }
-    const V cn = fmav(splat<V>(a.a), Tree<K>::sum(d), c);
 #pragma unroll
-    for (int q = 0; q < K; ++q) Mem<V>::store(a.x[q], i, x[q]);
-    Mem<V>::store(a.xc, i, cn);
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int q = 0; q < K; ++q) Mem<V>::store(a.x[q], i + I(u) * du, x[u][q]);
+        Mem<V>::store(a.xc, i + I(u) * du, c[u]);
+    }
 }
 
-template <typename T, typename V>
-__device__ __forceinline__ void easgd_slot_generic(const EasgdArgs<TC_MAX_K, T>& a, int64_t i) {
+template <typename T, typename V, typename I>
+__device__ __forceinline__ void easgd_slot_generic(const EasgdArgs<TC_MAX_K, T>& a, I i) {
     constexpr int kParts = TC_MAX_K / kSpecialisedK;
     const V c = Mem<V>::load(a.xc, i);
     const V rho = splat<V>(a.rho), neg_eta = splat<V>(-a.eta);
@@ -239,38 +250,60 @@ __device__ __forceinline__ void easgd_slot_generic(const EasgdArgs<TC_MAX_K, T>&
     Mem<V>::store(a.xc, i, fmav(splat<V>(a.a), Tree<kParts>::sum(part), c));
 }
 
-template <int K, typename T>
-__device__ __forceinline__ void easgd_any(const EasgdArgs<K, T>& a, int64_t i, f4) {
-    if constexpr (K == TC_MAX_K) easgd_slot_generic<T, f4>(a, i); else easgd_slot<K, T, f4>(a, i);
-}
-template <int K, typename T>
-__device__ __forceinline__ void easgd_any(const EasgdArgs<K, T>& a, int64_t i, float) {
-    if constexpr (K == TC_MAX_K) easgd_slot_generic<T, float>(a, i); else easgd_slot<K, T, float>(a, i);
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void easgd_any(const EasgdArgs<K, T>& a, I i, I du) {
+    if constexpr (K == TC_MAX_K) easgd_slot_generic<T, V, I>(a, i);
+    else easgd_slots<K, T, U, V, I>(a, i, du);
 }
 
-template <int K, typename T>
-__global__ __launch_bounds__(TC_EW_THREADS) void easgd_vec_kernel(EasgdArgs<K, T> a, int64_t nslot, int64_t n) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * TC_EW_THREADS;
-    for (int64_t s = static_cast<int64_t>(blockIdx.x) * TC_EW_THREADS + threadIdx.x; s < nslot; s += stride)
-        easgd_any<K, T>(a, s, f4{});
+// -------------------------------------------------------------- kernels
+
+// Op selects reduce or easgd through the argument type.
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void op_any(const ReduceArgs<K, T>& a, I i, I du) { reduce_any<K, T, U, V, I>(a, i, du); }
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void op_any(const EasgdArgs<K, T>& a, I i, I du) { easgd_any<K, T, U, V, I>(a, i, du); }
+
+// 16-byte slots, grid-stride; groups of U slots per lane, then the slots of
+// a last partial group one by one; the last workgroup does the < 4
+// trailing elements.
+template <int K, typename T, int U, typename I, template <int, typename> class Args>
+__global__ __launch_bounds__(TC_EW_THREADS) void vec_kernel(Args<K, T> a, I nslot, I n) {
+    constexpr int kU = (K == TC_MAX_K) ? 1 : U;
+    const I T_ = TC_EW_THREADS;
+    const I stride = static_cast<I>(gridDim.x) * T_ * kU;
+    I s = static_cast<I>(blockIdx.x) * T_ * kU + threadIdx.x;
+    for (; s + I(kU - 1) * T_ < nslot; s += stride) op_any<K, T, kU, f4, I>(a, s, T_);
+#pragma unroll
+    for (int u = 0; u < kU - 1; ++u)
+        if (s + I(u) * T_ < nslot) op_any<K, T, 1, f4, I>(a, s + I(u) * T_, T_);
     if (blockIdx.x == gridDim.x - 1) {
-        const int64_t j = 4 * nslot + threadIdx.x;
-        if (j < n) easgd_any<K, T>(a, j, 0.0f);
+        const I j = 4 * nslot + threadIdx.x;
+        if (j < n) op_any<K, T, 1, float, I>(a, j, I(1));
     }
 }
 
-template <int K, typename T>
-__global__ __launch_bounds__(TC_EW_THREADS) void easgd_scalar_kernel(EasgdArgs<K, T> a, int64_t n) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * TC_EW_THREADS;
-    for (int64_t j = static_cast<int64_t>(blockIdx.x) * TC_EW_THREADS + threadIdx.x; j < n; j += stride)
-        easgd_any<K, T>(a, j, 0.0f);
+// Element by element, grid-stride (buffers not 16-byte aligned).
+template <int K, typename T, typename I, template <int, typename> class Args>
+__global__ __launch_bounds__(TC_EW_THREADS) void scalar_kernel(Args<K, T> a, I n) {
+    const I stride = static_cast<I>(gridDim.x) * TC_EW_THREADS;
+    for (I j = static_cast<I>(blockIdx.x) * TC_EW_THREADS + threadIdx.x; j < n; j += stride)
+        op_any<K, T, 1, float, I>(a, j, I(1));
 }
 
 // -------------------------------------------------------------- launching
 
+// Slots per lane in flight (reduce, easgd).
+#ifndef TC_RD_UNROLL
+#define TC_RD_UNROLL 2
+#endif
+#ifndef TC_EA_UNROLL
+#define TC_EA_UNROLL 2
+#endif
+
 int g_cu_count = 0;
 
-int64_t grid_for(int64_t items) {
+int64_t grid_for(int64_t items, int per_lane) {
     if (g_cu_count == 0) {
         int dev = 0, cus = 0;
         if (hipGetDevice(&dev) == hipSuccess &&
@@ -279,9 +312,34 @@ int64_t grid_for(int64_t items) {
         else
             g_cu_count = 256;
     }
-    const int64_t want = (items + TC_EW_THREADS - 1) / TC_EW_THREADS;
+    const int64_t per_block = static_cast<int64_t>(TC_EW_THREADS) * per_lane;
+    const int64_t want = (items + per_block - 1) / per_block;
+    if (TC_EW_BLOCKS_PER_CU <= 0) return want < 1 ? 1 : want;
     const int64_t cap = static_cast<int64_t>(g_cu_count) * TC_EW_BLOCKS_PER_CU;
     return want < 1 ? 1 : (want < cap ? want : cap);
+}
+
+template <int K, typename T, int U, template <int, typename> class Args>
+hipError_t launch(const Args<K, T>& a, int64_t n, bool vec, int elem_bytes_max, hipStream_t s) {
+    // 32-bit byte offsets when the largest buffer is below 4 GiB
+    const bool off32 = n * elem_bytes_max < (int64_t(1) << 32) - 64;
+    if (vec) {
+        const int64_t nslot = n / 4;
+        dim3 grid(static_cast<unsigned>(grid_for(nslot, K == TC_MAX_K ? 1 : U)));
+        if (off32)
+            hipLaunchKernelGGL((vec_kernel<K, T, U, uint32_t, Args>), grid, dim3(TC_EW_THREADS), 0, s, a,
+                               static_cast<uint32_t>(nslot), static_cast<uint32_t>(n));
+        else
+            hipLaunchKernelGGL((vec_kernel<K, T, U, int64_t, Args>), grid, dim3(TC_EW_THREADS), 0, s, a, nslot, n);
+    } else {
+        dim3 grid(static_cast<unsigned>(grid_for(n, 1)));
+        if (off32)
+            hipLaunchKernelGGL((scalar_kernel<K, T, uint32_t, Args>), grid, dim3(TC_EW_THREADS), 0, s, a,
+                               static_cast<uint32_t>(n));
+        else
+            hipLaunchKernelGGL((scalar_kernel<K, T, int64_t, Args>), grid, dim3(TC_EW_THREADS), 0, s, a, n);
+    }
+    return hipGetLastError();
 }
 
 template <int K, typename T>
@@ -291,13 +349,7 @@ hipError_t run_reduce(const void* const* in, float* out, int op, int k_total, in
     a.out = out;
     a.op = op;
     a.k_total = k_total;
-    if (vec) {
-        const int64_t nslot = n / 4;
-        hipLaunchKernelGGL((reduce_vec_kernel<K, T>), dim3(grid_for(nslot)), dim3(TC_EW_THREADS), 0, s, a, nslot, n);
-    } else {
-        hipLaunchKernelGGL((reduce_scalar_kernel<K, T>), dim3(grid_for(n)), dim3(TC_EW_THREADS), 0, s, a, n);
-    }
-    return hipGetLastError();
+    return launch<K, T, TC_RD_UNROLL>(a, n, vec, 4, s);
 }
 
 template <int K, typename T>
@@ -313,13 +365,7 @@ hipError_t run_easgd(float* const* x, const void* const* g, float* xc, float eta
     a.rho = rho;
     a.a = eta * rho;  // one binary32 rounding, on the host
     a.k_total = k_total;
-    if (vec) {
-        const int64_t nslot = n / 4;
-        hipLaunchKernelGGL((easgd_vec_kernel<K, T>), dim3(grid_for(nslot)), dim3(TC_EW_THREADS), 0, s, a, nslot, n);
-    } else {
-        hipLaunchKernelGGL((easgd_scalar_kernel<K, T>), dim3(grid_for(n)), dim3(TC_EW_THREADS), 0, s, a, n);
-    }
-    return hipGetLastError();
+    return launch<K, T, TC_EA_UNROLL>(a, n, vec, 4, s);
 }
 
 #define TC_FOR_K(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)

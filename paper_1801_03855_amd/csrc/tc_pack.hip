@@ -2,18 +2,26 @@
 // copies' flat buffers, in one launch for all tensors and all copies.
 //
 // The flat index space is cut into chunks of kChunk elements; workgroup
-// (b, k) copies chunk b of copy k.  The host precomputed, for every chunk,
-// the first tensor it touches; the workgroup stages the offsets (relative to
-// the chunk, clamped to it) and pointers of the tensors overlapping its
-// chunk in LDS, so a group of thousands of small tensors costs one launch
-// and one table read per workgroup.  Each lane then owns 16-byte slots of
-// the flat side (coalesced 1 KiB per wave instruction), finds the tensor
-// holding the slot by binary search in LDS, and moves the slot with one
-// 16-byte access when it lies inside one tensor at a 16-byte aligned
-// address there, element by element otherwise (tensor boundaries, tensors
-// whose data is not 16-byte aligned, the ragged end of the group).  A chunk
-// touching more than kMaxStage tensors (only possible with many tiny or
-// empty tensors) searches the device tables in global memory instead.
+// (b, k) moves chunk b of copy k.  The host precomputed, for every chunk,
+// the first tensor it touches, so the workgroup reads one table entry and
+// stages the chunk-relative offsets and pointers of the tensors overlapping
+// its chunk (its "segments") in LDS: a group of thousands of small tensors
+// costs one launch.
+//
+// Work is enumerated over 16-byte aligned granules of the destination side
+// (the flat buffer for pack, the tensors for unpack): a prefix sum over the
+// segments' granule counts, in LDS, lets each lane find its granule by
+// binary search.  A granule lying wholly inside one segment is written with
+// one 16-byte store; its 16 source bytes are read with one 16-byte load when
+// they are aligned, else as the two aligned source granules that hold them,
+// funnel-shifted into place (both granules hold bytes of the source range,
+// so no read leaves the pages the source occupies).  Granules cut by a
+// segment's ends are copied element by element.  So tensors at any element
+// alignment, and any flat offset, move with full-width accesses.
+//
+// A chunk touching more than kMaxStage tensors (only possible with many
+// tiny or empty tensors) is copied element by element, searching the device
+// tables in global memory.
 #include "tc_internal.h"
 
 #ifndef TC_PACK_THREADS
@@ -25,6 +33,8 @@ namespace {
 
 typedef unsigned int u4 __attribute__((ext_vector_type(4)));
 
+constexpr int kWaves = TC_PACK_THREADS / 64;
+
 struct PackKernelArgs {
     const int64_t* offsets;
     const int32_t* chunk_first;
@@ -34,69 +44,99 @@ struct PackKernelArgs {
     void* flat[TC_MAX_K];
 };
 
-// Segment tables: relative offsets rel(0..nseg) (clamped to [0, clen]), the
-// true start of segment 0 relative to the chunk (<= 0), pointers ptr(s).
-struct LdsTable {
-    const int32_t* rel;
-    void* const* ptr;
-    __device__ int32_t r(int s) const { return rel[s]; }
-    __device__ void* p(int s) const { return ptr[s]; }
+__device__ __forceinline__ int32_t clamp_rel(int64_t v, int32_t clen) {
+    return static_cast<int32_t>(v < 0 ? 0 : (v > clen ? clen : v));
+}
+
+// Bytes [sh, sh + 16) of the 32-byte little-endian concatenation lo:hi.
+__device__ __forceinline__ u4 funnel(u4 lo, u4 hi, uint32_t sh) {
+    const uint32_t w[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    const uint32_t d4 = sh >> 2, b = sh & 3;
+    uint32_t t[5];
+#pragma unroll
+    for (int j = 0; j < 5; ++j)
+        t[j] = d4 == 0 ? w[j] : d4 == 1 ? w[j + 1] : d4 == 2 ? w[j + 2] : w[j + 3];
+    return u4{__builtin_amdgcn_alignbyte(t[1], t[0], b), __builtin_amdgcn_alignbyte(t[2], t[1], b),
+              __builtin_amdgcn_alignbyte(t[3], t[2], b), __builtin_amdgcn_alignbyte(t[4], t[3], b)};
+}
+
+// Destination byte range [d0, d1) of one segment's part of the chunk, and
+// the displacement from a destination byte to its source byte.
+struct SegView {
+    uintptr_t d0, d1;
+    intptr_t delta;
 };
 
-struct GlobalTable {
-    const int64_t* off;  // offsets + lo
-    void* const* ptr;    // copy's pointers + lo
-    int64_t cstart;
-    int32_t clen;
-    __device__ int32_t r(int s) const {
-        int64_t v = off[s] - cstart;
-        return static_cast<int32_t>(v < 0 ? 0 : (v > clen ? clen : v));
+template <typename T, bool UNPACK>
+__device__ __forceinline__ SegView seg_view(const int32_t* rel, const char* const* ptr, int s,
+                                            int64_t first_start, uintptr_t flat0) {
+    constexpr intptr_t es = sizeof(T);
+    const int32_t e0 = rel[s], e1 = rel[s + 1];
+    const int64_t start = s == 0 ? first_start : rel[s];
+    // byte address, in the tensor, of chunk-relative flat element 0
+    const uintptr_t tens0 = reinterpret_cast<uintptr_t>(ptr[s]) - static_cast<uintptr_t>(start * es);
+    SegView v;
+    if (UNPACK) {
+        v.d0 = tens0 + e0 * es;
+        v.d1 = tens0 + e1 * es;
+        v.delta = static_cast<intptr_t>(flat0 - tens0);
+    } else {
+        v.d0 = flat0 + e0 * es;
+        v.d1 = flat0 + e1 * es;
+        v.delta = static_cast<intptr_t>(tens0 - flat0);
     }
-    __device__ void* p(int s) const { return ptr[s]; }
-};
+    return v;
+}
 
-template <typename T, bool UNPACK, bool FLAT16, typename Table>
-__device__ __forceinline__ void copy_chunk(const Table& tab, int nseg, int64_t first_start, int32_t clen,
-                                           T* flat_chunk) {
-    constexpr int VEC = 16 / sizeof(T);
-    const int nvec = (clen + VEC - 1) / VEC;
-    for (int v = threadIdx.x; v < nvec; v += TC_PACK_THREADS) {
-        const int jr = v * VEC;
-        // last segment whose start is <= jr (rel(0) == 0 always qualifies)
-        int lo = 0, hi = nseg - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (tab.r(mid) <= jr) lo = mid; else hi = mid - 1;
+__device__ __forceinline__ int32_t granules(const SegView& v) {
+    if (v.d1 <= v.d0) return 0;
+    return static_cast<int32_t>(((v.d1 + 15) >> 4) - (v.d0 >> 4));
+}
+
+template <typename T>
+__device__ __forceinline__ void copy_granule(const SegView& v, uintptr_t A) {
+    constexpr uintptr_t es = sizeof(T);
+    const uintptr_t lo = A > v.d0 ? A : v.d0;
+    const uintptr_t hi = A + 16 < v.d1 ? A + 16 : v.d1;
+    if (lo == A && hi == A + 16) {
+        const uintptr_t S = A + v.delta;
+        u4 val;
+        if ((S & 15) == 0) {
+            val = __builtin_nontemporal_load(reinterpret_cast<const u4*>(S));
+        } else {
+            const u4* g = reinterpret_cast<const u4*>(S & ~uintptr_t(15));
+            val = funnel(g[0], g[1], static_cast<uint32_t>(S & 15));
         }
-        int s = lo;
-        int64_t start = s == 0 ? first_start : tab.r(s);
-        T* tp = static_cast<T*>(tab.p(s)) + (jr - start);
-        if (FLAT16 && jr + VEC <= tab.r(s + 1) &&
-            (reinterpret_cast<uintptr_t>(tp) & 15) == 0) {
-            u4* fv = reinterpret_cast<u4*>(flat_chunk + jr);
-            u4* tv = reinterpret_cast<u4*>(tp);
-            if (UNPACK) __builtin_nontemporal_store(__builtin_nontemporal_load(fv), tv);
-            else __builtin_nontemporal_store(__builtin_nontemporal_load(tv), fv);
-            continue;
-        }
-        const int cnt = clen - jr < VEC ? clen - jr : VEC;
-        for (int q = 0; q < cnt; ++q) {
-            const int jq = jr + q;
-            while (jq >= tab.r(s + 1)) {
-                ++s;
-                start = tab.r(s);
-            }
-            T* te = static_cast<T*>(tab.p(s)) + (jq - start);
-            if (UNPACK) *te = flat_chunk[jq];
-            else flat_chunk[jq] = *te;
-        }
+        __builtin_nontemporal_store(val, reinterpret_cast<u4*>(A));
+    } else {
+        for (uintptr_t x = lo; x < hi; x += es)
+            *reinterpret_cast<T*>(x) = *reinterpret_cast<const T*>(x + v.delta);
     }
 }
 
-template <typename T, bool UNPACK, bool FLAT16>
+// Element-by-element copy of a chunk whose segments stay in global memory.
+template <typename T, bool UNPACK>
+__device__ void copy_chunk_global(const int64_t* off, void* const* cp, int nseg, int64_t cstart, int32_t clen,
+                                  T* flat_chunk) {
+    for (int jr = threadIdx.x; jr < clen; jr += TC_PACK_THREADS) {
+        int lo = 0, hi = nseg - 1;  // last segment whose start is <= jr
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (clamp_rel(off[mid] - cstart, clen) <= jr) lo = mid; else hi = mid - 1;
+        }
+        T* te = static_cast<T*>(cp[lo]) + (cstart + jr - off[lo]);
+        if (UNPACK) *te = flat_chunk[jr];
+        else flat_chunk[jr] = *te;
+    }
+}
+
+template <typename T, bool UNPACK>
 __global__ __launch_bounds__(TC_PACK_THREADS) void pack_kernel(PackKernelArgs a) {
     __shared__ int32_t s_rel[kMaxStage + 1];
-    __shared__ void* s_ptr[kMaxStage];
+    __shared__ const char* s_ptr[kMaxStage];
+    __shared__ int32_t s_pre[kMaxStage + 1];
+    __shared__ int32_t s_wave[kWaves];
+    const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
     const int k = blockIdx.y;
     const int64_t cstart = b * kChunk;
@@ -105,35 +145,73 @@ __global__ __launch_bounds__(TC_PACK_THREADS) void pack_kernel(PackKernelArgs a)
     const int32_t hi = a.chunk_first[b + 1];
     const int nseg = hi - lo + 1;
     void* const* cp = a.ptrs + static_cast<int64_t>(k) * a.n + lo;
-    const int64_t first_start = a.offsets[lo] - cstart;
     T* flat_chunk = static_cast<T*>(a.flat[k]) + cstart;
-    if (nseg <= kMaxStage) {
-        for (int s = threadIdx.x; s <= nseg; s += TC_PACK_THREADS) {
-            int64_t v = a.offsets[lo + s] - cstart;
-            s_rel[s] = static_cast<int32_t>(v < 0 ? 0 : (v > clen ? clen : v));
-            if (s < nseg) s_ptr[s] = cp[s];
+    if (nseg > kMaxStage) {
+        copy_chunk_global<T, UNPACK>(a.offsets + lo, cp, nseg, cstart, clen, flat_chunk);
+        return;
+    }
+    const int64_t first_start = a.offsets[lo] - cstart;
+    for (int s = tid; s <= nseg; s += TC_PACK_THREADS) {
+        s_rel[s] = clamp_rel(a.offsets[lo + s] - cstart, clen);
+        if (s < nseg) s_ptr[s] = static_cast<const char*>(cp[s]);
+    }
+    __syncthreads();
+
+    // exclusive prefix sum of the segments' granule counts
+    const uintptr_t flat0 = reinterpret_cast<uintptr_t>(flat_chunk);
+    const int spt = (nseg + TC_PACK_THREADS - 1) / TC_PACK_THREADS;
+    int local = 0;
+    for (int i = 0; i < spt; ++i) {
+        const int s = tid * spt + i;
+        if (s < nseg) local += granules(seg_view<T, UNPACK>(s_rel, s_ptr, s, first_start, flat0));
+    }
+    const int lane = tid & 63, wid = tid >> 6;
+    int incl = local;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int o = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += o;
+    }
+    if (lane == 63) s_wave[wid] = incl;
+    __syncthreads();
+    int base = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        base += w < wid ? s_wave[w] : 0;
+        total += s_wave[w];
+    }
+    int run = base + incl - local;
+    for (int i = 0; i < spt; ++i) {
+        const int s = tid * spt + i;
+        if (s < nseg) {
+            s_pre[s] = run;
+            run += granules(seg_view<T, UNPACK>(s_rel, s_ptr, s, first_start, flat0));
         }
-        __syncthreads();
-        copy_chunk<T, UNPACK, FLAT16>(LdsTable{s_rel, s_ptr}, nseg, first_start, clen, flat_chunk);
-    } else {
-        copy_chunk<T, UNPACK, FLAT16>(GlobalTable{a.offsets + lo, cp, cstart, clen}, nseg, first_start, clen,
-                                      flat_chunk);
+    }
+    if (tid == 0) s_pre[nseg] = total;
+    __syncthreads();
+
+    for (int q = tid; q < total; q += TC_PACK_THREADS) {
+        int l = 0, h = nseg - 1;  // last segment whose prefix is <= q
+        while (l < h) {
+            const int mid = (l + h + 1) >> 1;
+            if (s_pre[mid] <= q) l = mid; else h = mid - 1;
+        }
+        const SegView v = seg_view<T, UNPACK>(s_rel, s_ptr, l, first_start, flat0);
+        copy_granule<T>(v, ((v.d0 >> 4) + static_cast<uintptr_t>(q - s_pre[l])) << 4);
     }
 }
 
 template <typename T, bool UNPACK>
-hipError_t run(const PackKernelArgs& a, int K, int64_t nchunks, bool flat16, hipStream_t s) {
+hipError_t run(const PackKernelArgs& a, int K, int64_t nchunks, hipStream_t s) {
     dim3 grid(static_cast<unsigned>(nchunks), static_cast<unsigned>(K));
-    if (flat16)
-        hipLaunchKernelGGL((pack_kernel<T, UNPACK, true>), grid, dim3(TC_PACK_THREADS), 0, s, a);
-    else
-        hipLaunchKernelGGL((pack_kernel<T, UNPACK, false>), grid, dim3(TC_PACK_THREADS), 0, s, a);
+    hipLaunchKernelGGL((pack_kernel<T, UNPACK>), grid, dim3(TC_PACK_THREADS), 0, s, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, bool flat_aligned,
+hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, bool /*flat_aligned*/,
                        hipStream_t stream) {
     const tc_group* g = tl->g;
     PackKernelArgs a{};
@@ -144,10 +222,10 @@ hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, 
     a.N = g->N;
     for (int k = 0; k < tl->K; ++k) a.flat[k] = flat[k];
     if (tl->elem == 2)
-        return unpack ? run<uint16_t, true>(a, tl->K, g->nchunks, flat_aligned, stream)
-                      : run<uint16_t, false>(a, tl->K, g->nchunks, flat_aligned, stream);
-    return unpack ? run<uint32_t, true>(a, tl->K, g->nchunks, flat_aligned, stream)
-                  : run<uint32_t, false>(a, tl->K, g->nchunks, flat_aligned, stream);
+        return unpack ? run<uint16_t, true>(a, tl->K, g->nchunks, stream)
+                      : run<uint16_t, false>(a, tl->K, g->nchunks, stream);
+    return unpack ? run<uint32_t, true>(a, tl->K, g->nchunks, stream)
+                  : run<uint32_t, false>(a, tl->K, g->nchunks, stream);
 }
 
 }  // namespace tc

@@ -396,13 +396,25 @@ def test_small_and_empty_lengths(orc, N):
         assert_close(host_f32(xc), rc, mc, "x_c")
 
 
-def _pack_roundtrip(orc, sizes, K, dtype, misalign=False, seed=0):
+def _pack_roundtrip(orc, sizes, K, dtype, misalign=False, seed=0, flat_shift=0, views=False):
+    """pack then unpack through the C ABI, both checked bit for bit against
+    the oracle.  misalign: every tensor starts one element past its
+    allocation; views: the tensors of a copy are adjacent views of one
+    buffer starting at an odd element (so neighbours share 16-byte
+    granules); flat_shift: the flat buffers start that many elements past
+    their allocation."""
     g = tc.Group(sizes)
     gen = torch.Generator(device=DEV).manual_seed(seed)
     tensors = []
     for _ in range(K):
         copy = []
-        for s in sizes:
+        if views:
+            buf = torch.randn(sum(sizes) + 3, generator=gen, device=DEV).to(dtype)
+            at = 3
+            for s in sizes:
+                copy.append(buf[at:at + s])
+                at += s
+        for s in ([] if views else sizes):
             if misalign:
                 t = torch.randn(s + 1, generator=gen, device=DEV).to(dtype)[1:]
             else:
@@ -410,14 +422,25 @@ def _pack_roundtrip(orc, sizes, K, dtype, misalign=False, seed=0):
             copy.append(t)
         tensors.append(copy)
     tl = tc.TensorList(g, tensors)
-    flats = [torch.empty(max(g.numel, 1), dtype=dtype, device=DEV)[:g.numel] for _ in range(K)]
+    flats = [torch.empty(g.numel + flat_shift + 1, dtype=dtype, device=DEV)[flat_shift:flat_shift + g.numel]
+             for _ in range(K)]
     tc.pack(tl, flats)
     torch.cuda.synchronize()
     for k in range(K):
         ref = orc.pack([host_stored(t) for t in tensors[k]]) if g.numel else np.zeros(0)
         if g.numel:
             assert_bits_equal(host_stored(flats[k]), ref, f"pack copy {k}")
-    outs = [[torch.full((s,), 7.0, device=DEV).to(dtype) for s in sizes] for _ in range(K)]
+    if views:
+        outs = []
+        for _ in range(K):
+            buf = torch.full((sum(sizes) + 5,), 7.0, device=DEV).to(dtype)
+            at, copy = 5, []
+            for s in sizes:
+                copy.append(buf[at:at + s])
+                at += s
+            outs.append(copy)
+    else:
+        outs = [[torch.full((s,), 7.0, device=DEV).to(dtype) for s in sizes] for _ in range(K)]
     tl2 = tc.TensorList(g, outs)
     tc.unpack(tl2, flats)
     torch.cuda.synchronize()
@@ -438,6 +461,26 @@ def test_pack_misaligned_tensors(orc, dtype):
     """Tensors starting one element past an allocation: element path."""
     sizes = [1, 7, 4096, 3, 5000, 0, 4, 12345]
     _pack_roundtrip(orc, sizes, 3, dtype, misalign=True, seed=1)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("flat_shift", [1, 2, 3])
+def test_pack_misaligned_flat_buffers(orc, dtype, flat_shift):
+    """Flat buffers 1-3 elements past a 16-byte boundary, tensors aligned and
+    misaligned."""
+    sizes = wl.many_small_sizes(300, seed=flat_shift)
+    _pack_roundtrip(orc, sizes, 2, dtype, seed=10 + flat_shift, flat_shift=flat_shift)
+    _pack_roundtrip(orc, sizes, 2, dtype, misalign=True, seed=20 + flat_shift, flat_shift=flat_shift)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_pack_adjacent_views(orc, dtype):
+    """Tensors that are adjacent views of one buffer at odd offsets: unpack
+    writes neighbouring tensors' bytes within the same 16-byte granules from
+    different lanes and workgroups."""
+    sizes = [1, 2, 3, 5, 8, 13, 4099, 1, 7, 4096, 4097, 0, 6, 9000, 1, 1, 1, 33]
+    _pack_roundtrip(orc, sizes, 3, dtype, seed=30, views=True)
+    _pack_roundtrip(orc, wl.many_small_sizes(500, seed=31), 2, dtype, seed=31, views=True, flat_shift=1)
 
 
 def test_pack_many_tiny_and_empty_tensors(orc):
