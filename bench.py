@@ -53,6 +53,38 @@ def op_bytes(op: str, K: int, N: int, s_g: int) -> int:
     raise ValueError(op)
 
 
+# Files whose contents define the kernels measured by the hardware counters.
+KERNEL_SOURCES = ("paper_1801_03855_amd/csrc/tc_elementwise.hip", "paper_1801_03855_amd/csrc/tc_pack.hip",
+                  "paper_1801_03855_amd/csrc/tc_internal.h", "paper_1801_03855_amd/build.py")
+
+
+def kernel_source_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary of this workload, or {} when there is none or the
+    kernels have changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.md")
+    if not os.path.exists(path):
+        return {}
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and (line.startswith("source_sha256") or line.startswith("traffic_bytes_")):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != kernel_source_sha():
+        return {}
+    return {k[len("traffic_bytes_"):]: int(v) for k, v in vals.items() if k.startswith("traffic_bytes_")}
+
+
 def cpu_baseline(wkey: str, ops, sample_elems: int = 30_000_000, min_seconds: float = 10.0,
                  max_reps: int = 20):
     """The oracle, as it is, on the first tensors of the group (at least
@@ -116,6 +148,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="resnet50_k8_pipeline", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="only run one plain device copy of 1 GiB (read 1 GiB, write 1 GiB), the known "
+                         "reference for scaling hardware byte counters, and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build models the K workers as K resident copies "
@@ -124,6 +159,16 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.calibration_copy:
+        src = torch.ones(256 << 20, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.add(src, 0.0, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes_read": src.numel() * 4,
+                          "calibration_copy_bytes_written": dst.numel() * 4}))
+        return
 
     import paper_1801_03855_amd as tc
     from paper_1801_03855_amd import workloads as wl
@@ -194,8 +239,10 @@ def main():
         kernels[op] = {"ms": round(per_op_ms[op], 5), "bytes": b, "GB/s": round(gbs, 1),
                        "frac": round(gbs / HBM_PEAK_GBS, 4)}
     dom = "easgd" if "easgd" in ops else max(ops, key=lambda o: per_op_ms[o])
+    traffic = recorded_traffic(args.workload).get(dom)
     roof = {"bound": "hbm", "kernel": dom, "achieved": kernels[dom]["GB/s"], "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": kernels[dom]["frac"], "traffic": None}
+            "unit": "GB/s", "frac": kernels[dom]["frac"], "traffic": traffic,
+            "algorithmic_bytes": kernels[dom]["bytes"], "avg_ms": kernels[dom]["ms"]}
 
     cpu = None
     if not args.no_cpu_baseline:
