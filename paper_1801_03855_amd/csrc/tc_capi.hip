@@ -84,9 +84,10 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         g->offsets[t + 1] = g->offsets[t] + sizes[t];
     }
     g->N = g->offsets[n];
-    g->nchunks = (g->N + kChunk - 1) / kChunk;
+    g->chunk = g->N / n >= TC_PACK_LARGE_MEAN ? TC_PACK_CHUNK_LARGE : TC_PACK_CHUNK_SMALL;
+    g->nchunks = (g->N + g->chunk - 1) / g->chunk;
     if (g->nchunks > INT32_MAX / 2) { set_error("group too large"); delete g; return nullptr; }
-    // chunk_first[b]: the tensor holding flat position b*kChunk, i.e. the
+    // chunk_first[b]: the tensor holding flat position b*chunk, i.e. the
     // last tensor whose offset is <= that position (zero-size tensors at the
     // same offset come before the one that holds it).  The final entry is
     // the tensor holding position N-1.
@@ -95,7 +96,7 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         auto it = std::upper_bound(g->offsets.begin(), g->offsets.begin() + n, j);
         return static_cast<int32_t>(it - g->offsets.begin()) - 1;
     };
-    for (int64_t b = 0; b < g->nchunks; ++b) g->chunk_first[b] = tensor_at(b * kChunk);
+    for (int64_t b = 0; b < g->nchunks; ++b) g->chunk_first[b] = tensor_at(b * g->chunk);
     g->chunk_first[g->nchunks] = g->N > 0 ? tensor_at(g->N - 1) : 0;
 
     hipError_t e = hipGetDevice(&g->device);

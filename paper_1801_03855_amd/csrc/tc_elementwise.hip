@@ -7,9 +7,9 @@
 // Mapping: one lane owns one 16-byte slot of every stream (4 binary32
 // values; 4 bfloat16 gradients are 8 bytes), so each wave instruction moves
 // 1 KiB (512 B for bfloat16) of contiguous memory per buffer.  A lane owns
-// two slots (one per half of its workgroup's tile) and issues the loads of
-// all 2K+1 streams of both before any arithmetic.  One workgroup per tile;
-// non-temporal loads and stores, since nothing is re-read.
+// U slots (U = 4, 2 or 1 as K grows) and issues the loads of all streams of
+// all of them before any arithmetic.  One workgroup per tile of 256*U
+// slots; non-temporal loads and stores, since nothing is re-read.
 // A ragged tail of fewer than 4 elements is handled element by element by
 // the last workgroup; buffers that are not 16-byte aligned take the
 // element-by-element kernel.
@@ -293,13 +293,11 @@ __global__ __launch_bounds__(TC_EW_THREADS) void scalar_kernel(Args<K, T> a, I n
 
 // -------------------------------------------------------------- launching
 
-// Slots per lane in flight (reduce, easgd).
-#ifndef TC_RD_UNROLL
-#define TC_RD_UNROLL 2
-#endif
-#ifndef TC_EA_UNROLL
-#define TC_EA_UNROLL 2
-#endif
+// Slots per lane in flight, by the number of streams: more slots for few
+// streams, one slot once a lane already has 2K+1 >= 17 loads in flight
+// (measured on MI355X; more costs occupancy without adding bandwidth).
+constexpr int reduce_unroll(int K) { return K <= 3 ? 4 : K <= 8 ? 2 : 1; }
+constexpr int easgd_unroll(int K) { return K <= 2 ? 4 : K <= 8 ? 2 : 1; }
 
 int g_cu_count = 0;
 
@@ -349,7 +347,7 @@ hipError_t run_reduce(const void* const* in, float* out, int op, int k_total, in
     a.out = out;
     a.op = op;
     a.k_total = k_total;
-    return launch<K, T, TC_RD_UNROLL>(a, n, vec, 4, s);
+    return launch<K, T, reduce_unroll(K)>(a, n, vec, 4, s);
 }
 
 template <int K, typename T>
@@ -365,7 +363,7 @@ hipError_t run_easgd(float* const* x, const void* const* g, float* xc, float eta
     a.rho = rho;
     a.a = eta * rho;  // one binary32 rounding, on the host
     a.k_total = k_total;
-    return launch<K, T, TC_EA_UNROLL>(a, n, vec, 4, s);
+    return launch<K, T, easgd_unroll(K)>(a, n, vec, 4, s);
 }
 
 #define TC_FOR_K(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)

@@ -13,8 +13,20 @@
 namespace tc {
 
 // Elements per pack/unpack chunk; one workgroup gathers or scatters one
-// chunk of one copy.  A multiple of every vector width used (4 and 8).
-constexpr int64_t kChunk = 4096;
+// chunk of one copy.  Chosen per group from its mean tensor size: groups of
+// large tensors (almost every chunk inside one tensor) move best in short
+// chunks that a workgroup covers in one batch per lane; groups of many small
+// tensors in long chunks, which spread the per-chunk segment staging over
+// more data (measured on MI355X).  Multiples of every vector width (4, 8).
+#ifndef TC_PACK_CHUNK_LARGE
+#define TC_PACK_CHUNK_LARGE 2048
+#endif
+#ifndef TC_PACK_CHUNK_SMALL
+#define TC_PACK_CHUNK_SMALL 8192
+#endif
+#ifndef TC_PACK_LARGE_MEAN
+#define TC_PACK_LARGE_MEAN 32768
+#endif
 
 // Segments (tensors overlapping one chunk) whose offsets and pointers a
 // workgroup stages in LDS; chunks touching more tensors search the global
@@ -46,7 +58,8 @@ struct tc_group {
     int device = 0;
     std::vector<int64_t> sizes;
     std::vector<int64_t> offsets;      // n + 1
-    int64_t nchunks = 0;               // ceil(N / kChunk)
+    int64_t chunk = 0;                 // elements per pack/unpack chunk
+    int64_t nchunks = 0;               // ceil(N / chunk)
     std::vector<int32_t> chunk_first;  // nchunks + 1
     int64_t* d_offsets = nullptr;
     int32_t* d_chunk_first = nullptr;

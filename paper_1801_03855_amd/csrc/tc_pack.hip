@@ -1,7 +1,7 @@
 // Pack / unpack between K copies of a group's separate tensors and the
 // copies' flat buffers, in one launch for all tensors and all copies.
 //
-// The flat index space is cut into chunks of kChunk elements; workgroup
+// The flat index space is cut into chunks (of the group's chunk length); workgroup
 // (b, k) moves chunk b of copy k.  The host precomputed, for every chunk,
 // the first tensor it touches, so the workgroup reads one table entry and
 // stages the chunk-relative offsets and pointers of the tensors overlapping
@@ -27,6 +27,11 @@
 #ifndef TC_PACK_THREADS
 #define TC_PACK_THREADS 256
 #endif
+// Granules a lane moves at a time: their loads are all issued before the
+// first store.
+#ifndef TC_PACK_BATCH
+#define TC_PACK_BATCH 2
+#endif
 
 namespace tc {
 namespace {
@@ -41,6 +46,7 @@ struct PackKernelArgs {
     void* const* ptrs;  // K*n device pointers, copy-major
     int32_t n;
     int64_t N;
+    int64_t chunk;
     void* flat[TC_MAX_K];
 };
 
@@ -93,25 +99,26 @@ __device__ __forceinline__ int32_t granules(const SegView& v) {
     return static_cast<int32_t>(((v.d1 + 15) >> 4) - (v.d0 >> 4));
 }
 
+// Whether destination granule A of segment v is whole (all 16 bytes inside
+// the segment's destination range).
+__device__ __forceinline__ bool whole(const SegView& v, uintptr_t A) { return A >= v.d0 && A + 16 <= v.d1; }
+
+// The 16 source bytes of a whole granule.
+__device__ __forceinline__ u4 load_granule(const SegView& v, uintptr_t A) {
+    const uintptr_t S = A + v.delta;
+    if ((S & 15) == 0) return __builtin_nontemporal_load(reinterpret_cast<const u4*>(S));
+    const u4* g = reinterpret_cast<const u4*>(S & ~uintptr_t(15));
+    return funnel(g[0], g[1], static_cast<uint32_t>(S & 15));
+}
+
+// Element-by-element copy of the part of granule A inside segment v.
 template <typename T>
-__device__ __forceinline__ void copy_granule(const SegView& v, uintptr_t A) {
+__device__ __forceinline__ void copy_partial(const SegView& v, uintptr_t A) {
     constexpr uintptr_t es = sizeof(T);
     const uintptr_t lo = A > v.d0 ? A : v.d0;
     const uintptr_t hi = A + 16 < v.d1 ? A + 16 : v.d1;
-    if (lo == A && hi == A + 16) {
-        const uintptr_t S = A + v.delta;
-        u4 val;
-        if ((S & 15) == 0) {
-            val = __builtin_nontemporal_load(reinterpret_cast<const u4*>(S));
-        } else {
-            const u4* g = reinterpret_cast<const u4*>(S & ~uintptr_t(15));
-            val = funnel(g[0], g[1], static_cast<uint32_t>(S & 15));
-        }
-        __builtin_nontemporal_store(val, reinterpret_cast<u4*>(A));
-    } else {
-        for (uintptr_t x = lo; x < hi; x += es)
-            *reinterpret_cast<T*>(x) = *reinterpret_cast<const T*>(x + v.delta);
-    }
+    for (uintptr_t x = lo; x < hi; x += es)
+        *reinterpret_cast<T*>(x) = *reinterpret_cast<const T*>(x + v.delta);
 }
 
 // Element-by-element copy of a chunk whose segments stay in global memory.
@@ -139,8 +146,8 @@ __global__ __launch_bounds__(TC_PACK_THREADS) void pack_kernel(PackKernelArgs a)
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
     const int k = blockIdx.y;
-    const int64_t cstart = b * kChunk;
-    const int32_t clen = static_cast<int32_t>(a.N - cstart < kChunk ? a.N - cstart : kChunk);
+    const int64_t cstart = b * a.chunk;
+    const int32_t clen = static_cast<int32_t>(a.N - cstart < a.chunk ? a.N - cstart : a.chunk);
     const int32_t lo = a.chunk_first[b];
     const int32_t hi = a.chunk_first[b + 1];
     const int nseg = hi - lo + 1;
@@ -157,48 +164,75 @@ __global__ __launch_bounds__(TC_PACK_THREADS) void pack_kernel(PackKernelArgs a)
     }
     __syncthreads();
 
-    // exclusive prefix sum of the segments' granule counts
+    // exclusive prefix sum of the segments' granule counts (a chunk inside
+    // one tensor, the common case for large tensors, needs none)
     const uintptr_t flat0 = reinterpret_cast<uintptr_t>(flat_chunk);
-    const int spt = (nseg + TC_PACK_THREADS - 1) / TC_PACK_THREADS;
-    int local = 0;
-    for (int i = 0; i < spt; ++i) {
-        const int s = tid * spt + i;
-        if (s < nseg) local += granules(seg_view<T, UNPACK>(s_rel, s_ptr, s, first_start, flat0));
-    }
-    const int lane = tid & 63, wid = tid >> 6;
-    int incl = local;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int o = __shfl_up(incl, d, 64);
-        if (lane >= d) incl += o;
-    }
-    if (lane == 63) s_wave[wid] = incl;
-    __syncthreads();
-    int base = 0, total = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-        base += w < wid ? s_wave[w] : 0;
-        total += s_wave[w];
-    }
-    int run = base + incl - local;
-    for (int i = 0; i < spt; ++i) {
-        const int s = tid * spt + i;
-        if (s < nseg) {
-            s_pre[s] = run;
-            run += granules(seg_view<T, UNPACK>(s_rel, s_ptr, s, first_start, flat0));
+    int total;
+    if (nseg == 1) {
+        total = granules(seg_view<T, UNPACK>(s_rel, s_ptr, 0, first_start, flat0));
+    } else {
+        const int spt = (nseg + TC_PACK_THREADS - 1) / TC_PACK_THREADS;
+        int local = 0;
+        for (int i = 0; i < spt; ++i) {
+            const int s = tid * spt + i;
+            if (s < nseg) local += granules(seg_view<T, UNPACK>(s_rel, s_ptr, s, first_start, flat0));
         }
+        const int lane = tid & 63, wid = tid >> 6;
+        int incl = local;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int o = __shfl_up(incl, d, 64);
+            if (lane >= d) incl += o;
+        }
+        if (lane == 63) s_wave[wid] = incl;
+        __syncthreads();
+        int base = 0;
+        total = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            base += w < wid ? s_wave[w] : 0;
+            total += s_wave[w];
+        }
+        int run = base + incl - local;
+        for (int i = 0; i < spt; ++i) {
+            const int s = tid * spt + i;
+            if (s < nseg) {
+                s_pre[s] = run;
+                run += granules(seg_view<T, UNPACK>(s_rel, s_ptr, s, first_start, flat0));
+            }
+        }
+        __syncthreads();
     }
-    if (tid == 0) s_pre[nseg] = total;
-    __syncthreads();
 
-    for (int q = tid; q < total; q += TC_PACK_THREADS) {
-        int l = 0, h = nseg - 1;  // last segment whose prefix is <= q
-        while (l < h) {
-            const int mid = (l + h + 1) >> 1;
-            if (s_pre[mid] <= q) l = mid; else h = mid - 1;
+    constexpr int B = TC_PACK_BATCH;
+    for (int q0 = tid; q0 < total; q0 += TC_PACK_THREADS * B) {
+        SegView v[B];
+        uintptr_t A[B];
+        bool full[B];
+        u4 val[B];
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+            const int q = q0 + i * TC_PACK_THREADS;
+            full[i] = false;
+            if (q < total) {
+                int l = 0, h = nseg - 1;  // last segment whose prefix is <= q
+                while (l < h) {
+                    const int mid = (l + h + 1) >> 1;
+                    if (s_pre[mid] <= q) l = mid; else h = mid - 1;
+                }
+                v[i] = seg_view<T, UNPACK>(s_rel, s_ptr, l, first_start, flat0);
+                const int pre = l == 0 ? 0 : s_pre[l];  // the first segment's prefix is 0
+                A[i] = ((v[i].d0 >> 4) + static_cast<uintptr_t>(q - pre)) << 4;
+                full[i] = whole(v[i], A[i]);
+                if (full[i]) val[i] = load_granule(v[i], A[i]);
+            }
         }
-        const SegView v = seg_view<T, UNPACK>(s_rel, s_ptr, l, first_start, flat0);
-        copy_granule<T>(v, ((v.d0 >> 4) + static_cast<uintptr_t>(q - s_pre[l])) << 4);
+#pragma unroll
+        for (int i = 0; i < B; ++i)
+            if (full[i]) __builtin_nontemporal_store(val[i], reinterpret_cast<u4*>(A[i]));
+#pragma unroll
+        for (int i = 0; i < B; ++i)
+            if (!full[i] && q0 + i * TC_PACK_THREADS < total) copy_partial<T>(v[i], A[i]);
     }
 }
 
@@ -220,6 +254,7 @@ hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, 
     a.ptrs = tl->d_ptrs;
     a.n = g->n;
     a.N = g->N;
+    a.chunk = g->chunk;
     for (int k = 0; k < tl->K; ++k) a.flat[k] = flat[k];
     if (tl->elem == 2)
         return unpack ? run<uint16_t, true>(a, tl->K, g->nchunks, stream)
