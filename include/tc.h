@@ -184,6 +184,53 @@ int32_t easgd_step_ex(const tc_group* g, int32_t K, float* const* x,
                       const void* const* grad, int32_t g_dtype, float* x_c,
                       float eta, float rho, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Tensor layout.  The paper's "tensor" (Sec. 6.1) is a grouping of vectors,
+ * one from each worker, operated on as one unit.  In this layout the K
+ * copies of a group live in ONE buffer, interleaved in slots of four
+ * consecutive elements: element e of copy i is at index
+ *
+ *     ((e / 4) * K + i) * 4 + (e % 4),
+ *
+ * so slot j holds, one after the other, the j-th four elements of copy 0,
+ * copy 1, ..., copy K-1.  The buffer holds tc_tensor_numel(g, K) =
+ * ceil(N/4) * 4 * K elements; when N is not a multiple of 4 the positions of
+ * e >= N in the last slot are padding, never read or written.  A K-way
+ * operation then reads one stream instead of K (on MI355X the fused step
+ * runs ~15% faster than on K separate buffers).  Results are the same as the
+ * separate-buffer entry points': the K-way sums use the same pairwise tree
+ * (bit-identical for power-of-two K, identical up to the sign of a zero
+ * otherwise).  Every buffer passed to these calls must be 16-byte aligned
+ * (TC_EINVAL otherwise).
+ * ---------------------------------------------------------------------- */
+
+/* Elements of a K-copy tensor-layout buffer of group g, or -1 on bad
+ * arguments. */
+int64_t tc_tensor_numel(const tc_group* g, int32_t K);
+
+/* Pack the K copies' separate tensors (the list's K*n tensors) into one
+ * tensor-layout buffer of the list's dtype (Sec. 3.2 push + Sec. 6.1
+ * tensor): tensor[((e/4)*K + k)*4 + e%4] = tensor(k, t)[e - offsets[t]] for
+ * the tensor t holding flat element e.  Bit for bit; one launch. */
+int32_t tc_pack_tensor(const tc_tensorlist* tl, void* tensor, void* stream);
+
+/* The inverse scatter (Sec. 3.2 pull): every copy's separate tensors from
+ * one tensor-layout buffer. */
+int32_t tc_unpack_tensor(const tc_tensorlist* tl, const void* tensor, void* stream);
+
+/* tc_reduce_ex on a tensor-layout input: out[e] = sum over i of copy i's
+ * element e (or that / K), for e < N.  in: K copies of in_dtype in the
+ * tensor layout; out: N binary32 values, not overlapping in. */
+int32_t tc_reduce_tensor(const tc_group* g, int32_t K, const void* in, int32_t in_dtype,
+                         float* out, int32_t op, void* stream);
+
+/* easgd_step_ex on tensor-layout workers and gradients: the same update,
+ * in place on x (K binary32 copies in the tensor layout) and x_c (N binary32
+ * values), with grad (K copies of g_dtype in the tensor layout).  The three
+ * buffers must not overlap. */
+int32_t easgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad,
+                          int32_t g_dtype, float* x_c, float eta, float rho, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -64,6 +64,12 @@ class Oracle:
                                           ctypes.POINTER(_VP), ctypes.c_int32, _DP,
                                           ctypes.c_double, ctypes.c_double]
         lib.oracle_easgd_step.restype = None
+        lib.oracle_tensor_from_copies.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(_VP),
+                                                  ctypes.c_int32, _VP]
+        lib.oracle_tensor_from_copies.restype = None
+        lib.oracle_copies_from_tensor.argtypes = [ctypes.c_int32, ctypes.c_int64, _VP, ctypes.c_int32,
+                                                  ctypes.POINTER(_VP)]
+        lib.oracle_copies_from_tensor.restype = None
         self.lib = lib
 
     # -- helpers --------------------------------------------------------
@@ -138,6 +144,27 @@ class Oracle:
         for _ in range(steps):
             self.lib.oracle_easgd_step(K, n, xp, gp, self._dtype_code(gs[0]),
                                        xc.ctypes.data_as(_DP), float(eta), float(rho))
+
+
+    # -- tensor layout ------------------------------------------------------
+    @staticmethod
+    def tensor_numel(N: int, K: int) -> int:
+        return (N + 3) // 4 * 4 * K
+
+    def tensor_from_copies(self, copies: Sequence[np.ndarray], fill=0) -> np.ndarray:
+        """One buffer holding the K copies in the tensor layout; padding
+        positions keep the value ``fill``."""
+        copies = [np.ascontiguousarray(c) for c in copies]
+        K, N, dt = len(copies), copies[0].size, copies[0].dtype
+        out = np.full(self.tensor_numel(N, K), fill, dtype=dt)
+        self.lib.oracle_tensor_from_copies(K, N, self._ptrs(copies), dt.itemsize, out.ctypes.data)
+        return out
+
+    def copies_from_tensor(self, tensor: np.ndarray, K: int, N: int) -> List[np.ndarray]:
+        tensor = np.ascontiguousarray(tensor)
+        outs = [np.empty(N, dtype=tensor.dtype) for _ in range(K)]
+        self.lib.oracle_copies_from_tensor(K, N, tensor.ctypes.data, tensor.dtype.itemsize, self._ptrs(outs))
+        return outs
 
 
 _DEFAULT: Optional[Oracle] = None

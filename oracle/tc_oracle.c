@@ -24,6 +24,11 @@
  *                   locally computed gradients; Sec. 3.2: push first sums
  *                   the tensors of one key; Sec. 5 (synchronous SGD): the
  *                   sum is rescaled by 1/mini_batch_size, i.e. averaged.
+ *   tensor layout   Sec. 6.1: a "tensor" is a grouping of vectors, one from
+ *                   each worker, handled as one unit.  Here the K copies
+ *                   are held in one buffer, interleaved in slots of four
+ *                   consecutive elements (an index map of this library's
+ *                   design, written out plainly below).
  *   easgd step      Sec. 2.1, Eq. (1) with dw = -eta * g (plain SGD);
  *                   Sec. 2.2, Eqs. (2) and (3) (elastic averaging: center
  *                   moves toward the worker, worker moves toward the center,
@@ -168,4 +173,39 @@ void oracle_easgd_step(int32_t K, int64_t N, double* const* x,
         }
         xc[j] = c + alpha * spread;
     }
+}
+
+/*
+ * Tensor layout of K copies of a group of N elements: element e of copy i
+ * sits at index ((e / 4) * K + i) * 4 + (e % 4) of one buffer of
+ * ceil(N / 4) * 4 * K elements.  Positions for e >= N are padding and are
+ * left untouched.
+ */
+static int64_t tensor_index(int32_t K, int64_t e, int32_t i)
+{
+    return ((e / 4) * K + i) * 4 + (e % 4);
+}
+
+/* Gather K flat copies into the tensor layout, bit for bit. */
+void oracle_tensor_from_copies(int32_t K, int64_t N, const void* const* copies,
+                               int32_t elem_bytes, void* tensor)
+{
+    unsigned char* dst = (unsigned char*)tensor;
+    for (int32_t i = 0; i < K; ++i)
+        for (int64_t e = 0; e < N; ++e)
+            memcpy(dst + tensor_index(K, e, i) * elem_bytes,
+                   (const unsigned char*)copies[i] + e * elem_bytes,
+                   (size_t)elem_bytes);
+}
+
+/* Scatter the tensor layout back into K flat copies, bit for bit. */
+void oracle_copies_from_tensor(int32_t K, int64_t N, const void* tensor,
+                               int32_t elem_bytes, void* const* copies)
+{
+    const unsigned char* src = (const unsigned char*)tensor;
+    for (int32_t i = 0; i < K; ++i)
+        for (int64_t e = 0; e < N; ++e)
+            memcpy((unsigned char*)copies[i] + e * elem_bytes,
+                   src + tensor_index(K, e, i) * elem_bytes,
+                   (size_t)elem_bytes);
 }

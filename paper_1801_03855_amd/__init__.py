@@ -12,6 +12,12 @@ loading fails loudly when the library has not been built.
     pack(tl, flats); unpack(tl, flats)      # tc_pack / tc_unpack
     reduce(g, ins, out, "avg")              # tc_reduce / tc_reduce_ex
     easgd_step(g, xs, gs, xc, eta, rho)     # easgd_step / easgd_step_ex
+
+Tensor layout (the K copies interleaved in one buffer):
+    n = tensor_numel(g, K)                  # tc_tensor_numel
+    pack_tensor(tl, T); unpack_tensor(tl, T)            # tc_pack_tensor / tc_unpack_tensor
+    reduce_tensor(g, K, T, out, "avg")      # tc_reduce_tensor
+    easgd_step_tensor(g, K, X, G, xc, eta, rho)         # easgd_step_tensor
 """
 
 from __future__ import annotations
@@ -72,6 +78,11 @@ def lib(path: str = LIBRARY) -> ctypes.CDLL:
         "tc_reduce_ex": (i32, [_VP, i32, _VPP, i32, _VP, i32, _VP]),
         "easgd_step": (i32, [_VP, i32, _VPP, _VPP, _VP, f32, f32, _VP]),
         "easgd_step_ex": (i32, [_VP, i32, _VPP, _VPP, i32, _VP, f32, f32, _VP]),
+        "tc_tensor_numel": (i64, [_VP, i32]),
+        "tc_pack_tensor": (i32, [_VP, _VP, _VP]),
+        "tc_unpack_tensor": (i32, [_VP, _VP, _VP]),
+        "tc_reduce_tensor": (i32, [_VP, i32, _VP, i32, _VP, i32, _VP]),
+        "easgd_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, _VP, f32, f32, _VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -219,3 +230,48 @@ def easgd_step(group: Group, xs: Sequence[torch.Tensor], gs: Sequence[torch.Tens
     _check(lib().easgd_step_ex(group.handle, len(xs), xp, gp, _DTYPES[gdt],
                                _dev_ptr(xc, n, (torch.float32,), "x_c"), float(eta), float(rho),
                                _stream(stream)))
+
+
+# --------------------------------------------------------------- tensor layout
+
+def tensor_numel(group: Group, K: int) -> int:
+    n = lib().tc_tensor_numel(group.handle, K)
+    if n < 0:
+        raise TCError(TC_EINVAL, f"bad K = {K}")
+    return n
+
+
+def pack_tensor(tl: TensorList, tensor: torch.Tensor, stream=None) -> None:
+    """K copies' separate tensors -> one tensor-layout buffer (tc_pack_tensor)."""
+    n = tensor_numel(tl.group, tl.K)
+    _check(lib().tc_pack_tensor(tl.handle, _dev_ptr(tensor, n, (tl.dtype,), "tensor"), _stream(stream)))
+
+
+def unpack_tensor(tl: TensorList, tensor: torch.Tensor, stream=None) -> None:
+    """One tensor-layout buffer -> the K copies' separate tensors (tc_unpack_tensor)."""
+    n = tensor_numel(tl.group, tl.K)
+    _check(lib().tc_unpack_tensor(tl.handle, _dev_ptr(tensor, n, (tl.dtype,), "tensor"), _stream(stream)))
+
+
+def reduce_tensor(group: Group, K: int, tensor: torch.Tensor, out: torch.Tensor, op="avg", stream=None) -> None:
+    """out = sum (or average) of the K copies in a tensor-layout buffer (tc_reduce_tensor)."""
+    dt = tensor.dtype
+    if dt not in _DTYPES:
+        raise TypeError(f"input has dtype {dt}")
+    p = _dev_ptr(tensor, tensor_numel(group, K), (dt,), "in")
+    _check(lib().tc_reduce_tensor(group.handle, K, p, _DTYPES[dt], _dev_ptr(out, group.numel, (torch.float32,), "out"),
+                                  _OPS[op], _stream(stream)))
+
+
+def easgd_step_tensor(group: Group, K: int, x: torch.Tensor, g: torch.Tensor, xc: torch.Tensor,
+                      eta: float, rho: float, stream=None) -> None:
+    """One fused elastic-averaging SGD step on tensor-layout workers x and
+    gradients g, in place on x and xc (easgd_step_tensor)."""
+    n = tensor_numel(group, K)
+    gdt = g.dtype
+    if gdt not in _DTYPES:
+        raise TypeError(f"gradients have dtype {gdt}")
+    _check(lib().easgd_step_tensor(group.handle, K, _dev_ptr(x, n, (torch.float32,), "x"),
+                                   _dev_ptr(g, n, (gdt,), "grad"), _DTYPES[gdt],
+                                   _dev_ptr(xc, group.numel, (torch.float32,), "x_c"), float(eta), float(rho),
+                                   _stream(stream)))

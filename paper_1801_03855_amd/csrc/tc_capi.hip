@@ -274,3 +274,71 @@ TC_API int32_t easgd_step(const tc_group* g, int32_t K, float* const* x, const f
                           float eta, float rho, void* stream) {
     return easgd_step_ex(g, K, x, reinterpret_cast<const void* const*>(grad), TC_F32, x_c, eta, rho, stream);
 }
+
+// ---------------------------------------------------------- tensor layout
+
+TC_API int64_t tc_tensor_numel(const tc_group* g, int32_t K) {
+    if (!g || K < 1 || K > TC_MAX_K) return -1;
+    return (g->N + 3) / 4 * 4 * K;
+}
+
+static int32_t tensor_pack_common(const tc_tensorlist* tl, void* tensor, bool unpack, void* stream) {
+    clear_error();
+    if (!tl) return fail(TC_EINVAL, "NULL tensor list");
+    const tc_group* g = tl->g;
+    if (int32_t r = check_device(g)) return r;
+    if (g->N == 0) return TC_OK;
+    if (!tensor) return fail(TC_EINVAL, "tensor is NULL");
+    if (!aligned(tensor, 16)) return fail(TC_EINVAL, "tensor buffers must be 16-byte aligned");
+    hipError_t e = launch_tensor_pack(tl, tensor, unpack, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, unpack ? "tc_unpack_tensor launch" : "tc_pack_tensor launch");
+    return TC_OK;
+}
+
+TC_API int32_t tc_pack_tensor(const tc_tensorlist* tl, void* tensor, void* stream) {
+    return tensor_pack_common(tl, tensor, false, stream);
+}
+
+TC_API int32_t tc_unpack_tensor(const tc_tensorlist* tl, const void* tensor, void* stream) {
+    return tensor_pack_common(tl, const_cast<void*>(tensor), true, stream);
+}
+
+TC_API int32_t tc_reduce_tensor(const tc_group* g, int32_t K, const void* in, int32_t in_dtype, float* out,
+                                int32_t op, void* stream) {
+    clear_error();
+    if (!g) return fail(TC_EINVAL, "group is NULL");
+    if (K < 1 || K > TC_MAX_K) { set_error("K = %d outside [1, %d]", K, TC_MAX_K); return TC_EINVAL; }
+    if (op != TC_SUM && op != TC_AVG) { set_error("unknown op %d", op); return TC_EINVAL; }
+    const int es = elem_size(in_dtype);
+    if (!es) { set_error("unknown dtype %d", in_dtype); return TC_EINVAL; }
+    if (int32_t r = check_device(g)) return r;
+    if (g->N == 0) return TC_OK;
+    if (!in || !out) return fail(TC_EINVAL, "NULL buffer");
+    if (!aligned(in, 16) || !aligned(out, 16)) return fail(TC_EINVAL, "tensor-layout calls need 16-byte aligned buffers");
+    if (overlap(in, tc_tensor_numel(g, K) * es, out, g->N * 4)) return fail(TC_EINVAL, "out overlaps the input tensor");
+    hipError_t e = launch_tensor_reduce(K, in, in_dtype, out, op, g->N, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "tc_reduce_tensor launch");
+    return TC_OK;
+}
+
+TC_API int32_t easgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad, int32_t g_dtype,
+                                 float* x_c, float eta, float rho, void* stream) {
+    clear_error();
+    if (!g) return fail(TC_EINVAL, "group is NULL");
+    if (K < 1 || K > TC_MAX_K) { set_error("K = %d outside [1, %d]", K, TC_MAX_K); return TC_EINVAL; }
+    const int es = elem_size(g_dtype);
+    if (!es) { set_error("unknown dtype %d", g_dtype); return TC_EINVAL; }
+    if (!std::isfinite(eta) || !std::isfinite(rho)) return fail(TC_EINVAL, "eta and rho must be finite");
+    if (int32_t r = check_device(g)) return r;
+    if (g->N == 0) return TC_OK;
+    if (!x || !grad || !x_c) return fail(TC_EINVAL, "NULL buffer");
+    if (!aligned(x, 16) || !aligned(grad, 16) || !aligned(x_c, 16))
+        return fail(TC_EINVAL, "tensor-layout calls need 16-byte aligned buffers");
+    const int64_t tn = tc_tensor_numel(g, K);
+    if (overlap(x, tn * 4, grad, tn * es)) return fail(TC_EINVAL, "x overlaps grad");
+    if (overlap(x, tn * 4, x_c, g->N * 4)) return fail(TC_EINVAL, "x overlaps x_c");
+    if (overlap(grad, tn * es, x_c, g->N * 4)) return fail(TC_EINVAL, "grad overlaps x_c");
+    hipError_t e = launch_tensor_easgd(K, x, grad, g_dtype, x_c, eta, rho, g->N, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "easgd_step_tensor launch");
+    return TC_OK;
+}

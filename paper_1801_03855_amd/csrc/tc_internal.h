@@ -44,9 +44,15 @@ hipError_t launch_reduce(int K, const void* const* in, int in_dtype, float* out,
 hipError_t launch_easgd(int K, float* const* x, const void* const* g, int g_dtype, float* xc,
                         float eta, float rho, int64_t n, bool vector_ok, hipStream_t stream);
 
-struct PackArgs;  // defined in tc_pack.hip
 hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, bool flat_aligned,
                        hipStream_t stream);
+
+// Tensor layout (K copies interleaved in slots of 4 elements).
+hipError_t launch_tensor_reduce(int K, const void* in, int in_dtype, float* out, int op, int64_t n,
+                                hipStream_t stream);
+hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, float* xc, float eta, float rho,
+                               int64_t n, hipStream_t stream);
+hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStream_t stream);
 
 }  // namespace tc
 

@@ -98,6 +98,31 @@ def pin_unpack_is_split(orc):
             assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
 
 
+def pin_tensor_layout_is_slot_transpose(orc):
+    """The tensor layout is numpy's (K, S, 4) -> (S, K, 4) transpose of the
+    copies zero-padded to S = ceil(N/4) slots, bit for bit; padding keeps
+    its fill; the inverse recovers the copies."""
+    rng = _rng(19)
+    for K, N in ((1, 9), (3, 10), (4, 16), (8, 37), (16, 1), (5, 4)):
+        for dtype in (np.float32, np.uint16):
+            copies = _tensors(rng, [N] * K, dtype)
+            S = (N + 3) // 4
+            padded = np.zeros((K, S * 4), dtype=dtype)
+            for i, c in enumerate(copies):
+                padded[i, :N] = c
+            ref = padded.reshape(K, S, 4).transpose(1, 0, 2).reshape(-1)
+            got = orc.tensor_from_copies(copies, fill=0)
+            assert np.array_equal(got.view(np.uint8), ref.view(np.uint8)), (K, N, dtype)
+            back = orc.copies_from_tensor(got, K, N)
+            for a, b in zip(back, copies):
+                assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), (K, N)
+            filled = orc.tensor_from_copies(copies, fill=7)
+            mask = np.zeros((K, S * 4), dtype=bool)
+            mask[:, N:] = True
+            mask = mask.reshape(K, S, 4).transpose(1, 0, 2).reshape(-1)
+            assert np.all(filled[mask] == 7) and np.array_equal(filled[~mask], ref[~mask])
+
+
 # ----------------------------------------------------------------- bf16
 
 def pin_bf16_decode_all_codes(orc):

@@ -51,6 +51,8 @@ MUTANTS = [
      "x[i][j] = xi - eta * (gi + rho * (xi - (c + alpha * spread)));"),
     ("worker_uses_other_gradient", "double gi = stored_value(g[i], g_dtype, j);",
      "double gi = stored_value(g[K - 1 - i], g_dtype, j);"),
+    ("tensor_slot_width", "return ((e / 4) * K + i) * 4 + (e % 4);", "return ((e / 2) * K + i) * 2 + (e % 2);"),
+    ("tensor_worker_major", "return ((e / 4) * K + i) * 4 + (e % 4);", "return (i * ((e / 4) + 1) + (e / 4)) * 4 + (e % 4);"),
     ("center_reads_new_workers",
      "        for (int32_t i = 0; i < K; ++i)\n            spread += x[i][j] - c;\n",
      ""),
