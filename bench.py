@@ -3,11 +3,18 @@
 One step is one pass of the whole path over a ResNet-50 v1 parameter group
 (161 tensors, 25,557,032 binary32 elements) with K = 8 worker copies:
 
-  1. tc_pack     the K workers' per-layer gradient tensors -> K flat buffers
-  2. tc_reduce   AVG of the K flat gradients (the synchronous tensor average)
-  3. easgd_step  fused center reduction + elastic + SGD update of the K flat
-                 worker copies and the center (eta = 0.05, rho = 0.9/(K eta))
-  4. tc_unpack   the K flat worker copies -> per-layer parameter tensors
+  1. pack     the K workers' per-layer gradient tensors -> the K copies'
+              group buffer(s)
+  2. reduce   AVG over the K gradient copies (the synchronous tensor average)
+  3. easgd    fused center reduction + elastic + SGD update of the K worker
+              copies and the center (eta = 0.05, rho = 0.9/(K eta))
+  4. unpack   the K worker copies -> per-layer parameter tensors
+
+The K copies are held either in the tensor layout (one buffer, copies
+interleaved in slots of four elements: tc_pack_tensor, tc_reduce_tensor,
+easgd_step_tensor, tc_unpack_tensor), the headline, or as K separate flat
+buffers (tc_pack, tc_reduce, easgd_step, tc_unpack), measured in the same
+run and reported beside it.  The bytes moved are the same.
 
 Inputs are seeded synthetic values resident in HBM before timing starts.
 The reported value is the step's algorithmic HBM traffic (every input read
@@ -17,6 +24,7 @@ The CPU baseline times the oracle (single thread) on a bounded sample of the
 same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--layout tensor|separate] [--no-compare]
 """
 
 from __future__ import annotations
@@ -33,11 +41,14 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 
 WORKLOADS = {
-    # name -> (workload key in paper_1801_03855_amd.workloads, ops per step)
-    "resnet50_k8_pipeline": ("resnet50_k8_easgd", ("pack", "reduce", "easgd", "unpack")),
-    "vgg16_k4_pipeline": ("vgg16_k4_easgd", ("pack", "reduce", "easgd", "unpack")),
-    "many_small_k16_bf16_pipeline": ("many_small_k16_bf16", ("pack", "reduce", "easgd", "unpack")),
+    # name -> (workload key in paper_1801_03855_amd.workloads, ops per step, default layout)
+    "resnet50_k8_pipeline": ("resnet50_k8_easgd", ("pack", "reduce", "easgd", "unpack"), "tensor"),
+    "vgg16_k4_pipeline": ("vgg16_k4_easgd", ("pack", "reduce", "easgd", "unpack"), "tensor"),
+    # 10,000 mostly misaligned tensors and K = 16 bfloat16 copies: the
+    # separate buffers pack and unpack faster than the interleaved tensor
+    "many_small_k16_bf16_pipeline": ("many_small_k16_bf16", ("pack", "reduce", "easgd", "unpack"), "separate"),
 }
+LAYOUTS = ("tensor", "separate")
 
 
 def op_bytes(op: str, K: int, N: int, s_g: int) -> int:
@@ -55,7 +66,8 @@ def op_bytes(op: str, K: int, N: int, s_g: int) -> int:
 
 # Files whose contents define the kernels measured by the hardware counters.
 KERNEL_SOURCES = ("paper_1801_03855_amd/csrc/tc_elementwise.hip", "paper_1801_03855_amd/csrc/tc_pack.hip",
-                  "paper_1801_03855_amd/csrc/tc_internal.h", "paper_1801_03855_amd/build.py")
+                  "paper_1801_03855_amd/csrc/tc_tensor.hip", "paper_1801_03855_amd/csrc/tc_internal.h",
+                  "paper_1801_03855_amd/build.py")
 
 
 def kernel_source_sha() -> str:
@@ -67,11 +79,11 @@ def kernel_source_sha() -> str:
     return h.hexdigest()
 
 
-def recorded_traffic(workload: str):
+def recorded_traffic(workload: str, layout: str):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE /
-    WRITE_SIZE summary of this workload, or {} when there is none or the
-    kernels have changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.md")
+    WRITE_SIZE summary of this workload and layout, or {} when there is none
+    or the kernels have changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_{layout}_hbm_traffic.md")
     if not os.path.exists(path):
         return {}
     vals = {}
@@ -141,12 +153,82 @@ def cpu_baseline(wkey: str, ops, sample_elems: int = 30_000_000, min_seconds: fl
             "steps_per_s": round(reps * n / (secs * sum(sizes)), 4)}
 
 
+def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
+    """Set up one layout's buffers, warm up, time `steps` steps; returns the
+    average step and per-op times (ms) from HIP events on the stream."""
+    import torch
+
+    N, K = g.numel, w.K
+    dev = "cuda"
+    gdt = torch.bfloat16 if w.g_dtype == "bf16" else torch.float32
+    print(f"# setup {name} ({layout} layout): n={len(sizes)} N={N} K={K}", file=sys.stderr, flush=True)
+    g_tensors = [wl.separate_tensors(f, sizes) for f in wl.make_gradients(w, N, dev)]
+    g_tl = tc.TensorList(g, g_tensors)
+    xs, xc = wl.make_state(w, N, dev)
+    gbar = torch.empty(N, dtype=torch.float32, device=dev)
+    x_tensors = [[torch.empty(s, dtype=torch.float32, device=dev) for s in sizes] for _ in range(K)]
+    x_tl = tc.TensorList(g, x_tensors)
+    stream = torch.cuda.current_stream()
+    if layout == "tensor":
+        G = torch.empty(tc.tensor_numel(g, K), dtype=gdt, device=dev)
+        X = torch.empty(tc.tensor_numel(g, K), dtype=torch.float32, device=dev)
+        tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X, stream)
+        del xs
+
+        def run_op(op):
+            if op == "pack":
+                tc.pack_tensor(g_tl, G, stream)
+            elif op == "reduce":
+                tc.reduce_tensor(g, K, G, gbar, "avg", stream)
+            elif op == "easgd":
+                tc.easgd_step_tensor(g, K, X, G, xc, w.eta, w.rho, stream)
+            elif op == "unpack":
+                tc.unpack_tensor(x_tl, X, stream)
+    else:
+        gflat = [torch.empty(N, dtype=gdt, device=dev) for _ in range(K)]
+
+        def run_op(op):
+            if op == "pack":
+                tc.pack(g_tl, gflat, stream)
+            elif op == "reduce":
+                tc.reduce(g, gflat, gbar, "avg", stream)
+            elif op == "easgd":
+                tc.easgd_step(g, xs, gflat, xc, w.eta, w.rho, stream)
+            elif op == "unpack":
+                tc.unpack(x_tl, xs, stream)
+
+    for _ in range(warmup):
+        for op in ops:
+            run_op(op)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        ev[s][0].record(stream)
+        for i, op in enumerate(ops):
+            run_op(op)
+            ev[s][i + 1].record(stream)
+    torch.cuda.synchronize()
+    print(f"# {layout}: timed {steps} steps in {time.perf_counter() - t0:.3f} s", file=sys.stderr, flush=True)
+    per_op_ms = {op: sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(steps)) / steps
+                 for i, op in enumerate(ops)}
+    step_ms = sum(ev[s][0].elapsed_time(ev[s][len(ops)]) for s in range(steps)) / steps
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return {"step_ms": step_ms, "per_op_ms": per_op_ms}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="resnet50_k8_pipeline", choices=sorted(WORKLOADS))
+    ap.add_argument("--layout", default=None, choices=LAYOUTS,
+                    help="how the K copies are held: one interleaved buffer (tensor) or K buffers "
+                         "(default: the workload's faster one)")
+    ap.add_argument("--no-compare", action="store_true", help="skip the other layout")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="only run one plain device copy of 1 GiB (read 1 GiB, write 1 GiB), the known "
@@ -173,76 +255,42 @@ def main():
     import paper_1801_03855_amd as tc
     from paper_1801_03855_amd import workloads as wl
 
-    wkey, ops = WORKLOADS[args.workload]
+    wkey, ops, default_layout = WORKLOADS[args.workload]
     w = wl.WORKLOADS[wkey]
-    dev = "cuda"
     torch.cuda.set_device(0)
     sizes = w.sizes()
     g = tc.Group(sizes)
     N, K = g.numel, w.K
-    gdt = torch.bfloat16 if w.g_dtype == "bf16" else torch.float32
     s_g = 2 if w.g_dtype == "bf16" else 4
 
-    print(f"# setup {args.workload}: n={len(sizes)} N={N} K={K}", file=sys.stderr, flush=True)
-    g_tensors = [wl.separate_tensors(f, sizes) for f in wl.make_gradients(w, N, dev)]
-    g_tl = tc.TensorList(g, g_tensors)
-    gflat = [torch.empty(N, dtype=gdt, device=dev) for _ in range(K)]
-    xs, xc = wl.make_state(w, N, dev)
-    gbar = torch.empty(N, dtype=torch.float32, device=dev)
-    x_tensors = [[torch.empty(s, dtype=torch.float32, device=dev) for s in sizes] for _ in range(K)]
-    x_tl = tc.TensorList(g, x_tensors)
-    stream = torch.cuda.current_stream()
-
-    def run_op(op):
-        if op == "pack":
-            tc.pack(g_tl, gflat, stream)
-        elif op == "reduce":
-            tc.reduce(g, gflat, gbar, "avg", stream)
-        elif op == "easgd":
-            tc.easgd_step(g, xs, gflat, xc, w.eta, w.rho, stream)
-        elif op == "unpack":
-            tc.unpack(x_tl, xs, stream)
-
-    for _ in range(args.warmup):
-        for op in ops:
-            run_op(op)
-    torch.cuda.synchronize()
-    print(f"# warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
-
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        ev[s][0].record(stream)
-        for i, op in enumerate(ops):
-            run_op(op)
-            ev[s][i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    print(f"# timed {args.steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
-
-    per_op_ms = {op: 0.0 for op in ops}
-    step_ms = 0.0
-    for s in range(args.steps):
-        for i, op in enumerate(ops):
-            per_op_ms[op] += ev[s][i].elapsed_time(ev[s][i + 1])
-        step_ms += ev[s][0].elapsed_time(ev[s][len(ops)])
-    per_op_ms = {op: v / args.steps for op, v in per_op_ms.items()}
-    step_ms /= args.steps
+    first = args.layout or default_layout
+    results = {first: run_pipeline(tc, wl, w, sizes, g, ops, first, args.steps, args.warmup, args.workload)}
+    if not args.no_compare:
+        other = [l for l in LAYOUTS if l != first][0]
+        results[other] = run_pipeline(tc, wl, w, sizes, g, ops, other, args.steps, args.warmup, args.workload)
+    step_ms = results[first]["step_ms"]
+    per_op_ms = results[first]["per_op_ms"]
     step_bytes = sum(op_bytes(op, K, N, s_g) for op in ops)
     value = step_bytes / (step_ms * 1e-3) / 1e9
 
-    kernels = {}
-    for op in ops:
-        b = op_bytes(op, K, N, s_g)
-        gbs = b / (per_op_ms[op] * 1e-3) / 1e9
-        kernels[op] = {"ms": round(per_op_ms[op], 5), "bytes": b, "GB/s": round(gbs, 1),
-                       "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    def kernel_table(pm):
+        out = {}
+        for op in ops:
+            b = op_bytes(op, K, N, s_g)
+            gbs = b / (pm[op] * 1e-3) / 1e9
+            out[op] = {"ms": round(pm[op], 5), "bytes": b, "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+        return out
+
+    kernels = kernel_table(per_op_ms)
     dom = "easgd" if "easgd" in ops else max(ops, key=lambda o: per_op_ms[o])
-    traffic = recorded_traffic(args.workload).get(dom)
-    roof = {"bound": "hbm", "kernel": dom, "achieved": kernels[dom]["GB/s"], "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": kernels[dom]["frac"], "traffic": traffic,
+    traffic = recorded_traffic(args.workload, first).get(dom)
+    roof = {"bound": "hbm", "kernel": f"{dom} ({first} layout)", "achieved": kernels[dom]["GB/s"],
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels[dom]["frac"], "traffic": traffic,
             "algorithmic_bytes": kernels[dom]["bytes"], "avg_ms": kernels[dom]["ms"]}
+    layouts = {}
+    for lay, r in results.items():
+        layouts[lay] = {"value": round(step_bytes / (r["step_ms"] * 1e-3) / 1e9, 2), "ms_per_step": round(r["step_ms"], 5),
+                        "kernels": kernel_table(r["per_op_ms"])}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -264,8 +312,9 @@ def main():
         "dtype": "f32" if s_g == 4 else "f32 (bf16 gradients)",
         "data": "synthetic (seeded; group shapes only, no weights or datasets)",
         "config": {"workload": args.workload, "group": w.group, "n_tensors": len(sizes), "N": N, "K": K,
-                   "ops": list(ops), "eta": w.eta, "rho": w.rho, "step_bytes": step_bytes},
+                   "layout": first, "ops": list(ops), "eta": w.eta, "rho": w.rho, "step_bytes": step_bytes},
         "kernels": kernels,
+        "layouts": layouts,
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -20,10 +20,6 @@
 // is done element by element by the last workgroup.
 #include "tc_internal.h"
 
-#ifndef TC_TP_BATCH
-#define TC_TP_BATCH 2
-#endif
-
 namespace tc {
 namespace {
 
@@ -54,6 +50,46 @@ __device__ __forceinline__ float group_sum(float v) {
     if constexpr (P >= 32) v = v + __shfl_xor(v, 16, 64);
     if constexpr (P >= 64) v = v + __shfl_xor(v, 32, 64);
     return v;
+}
+
+// Two-input DPP: lanes in the enabled banks (groups of 4 lanes of a row)
+// take CTRL's source lane from src, the others keep old.
+template <int CTRL, int BANKS>
+__device__ __forceinline__ float dpp_banks(float old, float src) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
+                                                                  __builtin_bit_cast(int, src), CTRL, 0xF, BANKS,
+                                                                  false));
+}
+
+// Split group sum of the four components of v over each aligned group of P
+// (>= 4) lanes.  Partner l^1 exchanges halves (lane bit 0 keeps components
+// {0,1} or {2,3}), partner l^2 exchanges quarters (bit 1 picks one of the
+// two), so after two steps each lane carries one component, and the
+// remaining steps add whole groups: l^4 (row rotates by 12 and by 4, each
+// written to the banks it serves), l^8 (row rotate by 8), l^16, l^32.  The
+// terms meet in the order of the pairwise tree, as in group_sum; each lane
+// ends with component comp_of_lane(l) of the group's sum, a quarter of the
+// work of summing all four components in every lane.
+__device__ __forceinline__ int comp_of_lane(int lane) { return ((lane & 1) << 1) | ((lane >> 1) & 1); }
+
+template <int P>
+__device__ __forceinline__ float split_group_sum(f4 v, int lane) {
+    static_assert(P >= 4, "two split steps need four lanes");
+    const bool b = lane & 1, c = (lane >> 1) & 1;
+    const float k0 = b ? v.z : v.x, k1 = b ? v.w : v.y;      // kept half
+    const float s0 = b ? v.x : v.z, s1 = b ? v.y : v.w;      // half for the partner
+    const float w0 = k0 + dpp<0xB1>(s0), w1 = k1 + dpp<0xB1>(s1);
+    float u = (c ? w1 : w0) + dpp<0x4E>(c ? w0 : w1);
+    if constexpr (P >= 8) {
+        // lane ^ 4: banks 0 and 2 read lane + 4 (rotate by 12), banks 1 and 3
+        // read lane - 4 (rotate by 4)
+        const float t = dpp_banks<0x12C, 0x5>(u, u);
+        u = u + dpp_banks<0x124, 0xA>(t, u);
+    }
+    if constexpr (P >= 16) u = u + dpp<0x128>(u);  // row_ror:8 = lane ^ 8
+    if constexpr (P >= 32) u = u + __shfl_xor(u, 16, 64);
+    if constexpr (P >= 64) u = u + __shfl_xor(u, 32, 64);
+    return u;
 }
 
 template <int P>
@@ -102,6 +138,16 @@ struct Tree<1> {
     static __device__ __forceinline__ float sum(float* v) { return v[0]; }
 };
 
+// First slot of this lane: a workgroup covers 4*U*(64/P) consecutive
+// slots, each wave U*(64/P) of them, so the single-stream outputs (the
+// reduction, the center) leave every wave as >= 128 contiguous bytes.
+template <int P, int U, typename I>
+__device__ __forceinline__ I first_slot() {
+    constexpr int SPW = 64 / P;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    return static_cast<I>(blockIdx.x) * (4 * U * SPW) + static_cast<I>(wave * U * SPW + lane / P);
+}
+
 // ------------------------------------------------------------- reduce
 
 template <typename T>
@@ -115,23 +161,32 @@ struct TReduceArgs {
 // P: lanes per slot (K rounded up to a power of two).
 template <int P, typename T, int U, typename I>
 __global__ __launch_bounds__(256) void tensor_reduce_kernel(TReduceArgs<T> a) {
-    constexpr int SPB = 256 / P;  // slots per workgroup and unroll step
+    constexpr int SPW = 64 / P;  // slots per wave and unroll step
     const int K = a.K;
     const int i = threadIdx.x % P;
-    const I j0 = static_cast<I>(blockIdx.x) * SPB * U + threadIdx.x / P;
+    const I j0 = first_slot<P, U, I>();
     const I nslot = static_cast<I>(a.nslot);
     f4 v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        const I j = j0 + I(u) * SPB;
+        const I j = j0 + I(u) * SPW;
         v[u] = (j < nslot && i < K) ? load_slot(a.in, j * I(K) + I(i)) : f4(0.0f);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        const I j = j0 + I(u) * SPB;
-        f4 s = group_sum4<P>(v[u]);
-        if (a.op == TC_AVG) s = s / f4(static_cast<float>(K));  // correctly rounded
-        if (j < nslot && i == 0) store_slot(a.out, j, s);
+        const I j = j0 + I(u) * SPW;
+        if constexpr (P >= 4) {
+            // lanes 0-3 of the group hold one component each
+            float s = split_group_sum<P>(v[u], threadIdx.x);
+            if (a.op == TC_AVG) s = s / static_cast<float>(K);  // correctly rounded
+            if (j < nslot && i < 4)
+                __builtin_nontemporal_store(s, reinterpret_cast<float*>(reinterpret_cast<char*>(a.out) + j * I(16)) +
+                                                   comp_of_lane(i));
+        } else {
+            f4 s = group_sum4<P>(v[u]);
+            if (a.op == TC_AVG) s = s / f4(static_cast<float>(K));  // correctly rounded
+            if (j < nslot && i == 0) store_slot(a.out, j, s);
+        }
     }
     if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot
         const int64_t e = 4 * a.nslot + threadIdx.x;
@@ -161,15 +216,15 @@ struct TEasgdArgs {
 
 template <int P, typename T, int U, typename I>
 __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
-    constexpr int SPB = 256 / P;
+    constexpr int SPW = 64 / P;
     const int K = a.K;
     const int i = threadIdx.x % P;
-    const I j0 = static_cast<I>(blockIdx.x) * SPB * U + threadIdx.x / P;
+    const I j0 = first_slot<P, U, I>();
     const I nslot = static_cast<I>(a.nslot);
     f4 x[U], g[U], c[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        const I j = j0 + I(u) * SPB;
+        const I j = j0 + I(u) * SPW;
         const bool slot = j < nslot;
         c[u] = slot ? load_slot(a.xc, j) : f4(0.0f);
         const bool live = slot && i < K;
@@ -179,7 +234,7 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
     const f4 rho = f4(a.rho), neg_eta = f4(-a.eta), alpha = f4(a.a);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        const I j = j0 + I(u) * SPB;
+        const I j = j0 + I(u) * SPW;
         const bool live = j < nslot && i < K;
         const f4 d = live ? x[u] - c[u] : f4(0.0f);
         const f4 xn = fma4(neg_eta, fma4(rho, d, g[u]), x[u]);
@@ -258,40 +313,57 @@ __device__ __forceinline__ void store_bytes(uintptr_t D, u4 v) {
     else __builtin_nontemporal_store(u2{v.x, v.y}, reinterpret_cast<u2*>(D));
 }
 
-// Workgroup b moves chunk b of all K copies.  Pieces (slot, copy) are
-// enumerated in tensor order, so the tensor side of every wave instruction
-// is contiguous; the per-worker side reads or writes 4 elements of one
-// copy's tensors, with one access when they lie in one tensor (funnel-
-// shifted when misaligned on the read side), element by element otherwise.
-template <typename T, bool UNPACK>
+// Workgroup b moves chunk b of all K copies through LDS, M slots at a time
+// (M = 1024/P, at least 16: a 16 KB tile for binary32), so that both global
+// sides are contiguous:
+//   per-copy side  lanes take consecutive slots of one copy (M*SB bytes of
+//                  one copy per wave instruction when M >= 64);
+//   tensor side    lanes take consecutive pieces in tensor order.
+// The tile rows (one per slot, K pieces of SB bytes) are padded by one
+// piece so the per-copy phase hits distinct LDS banks.  The chunk's
+// segments (tensors) are staged in LDS as chunk-relative starts and, per
+// copy, the address of chunk element 0 in that copy's tensor coordinates.
+// On the per-copy side a slot inside one tensor moves as one access:
+//   pack    one load, or the two aligned granules holding the bytes,
+//           funnel-shifted;
+//   unpack  one store when aligned; else the lane stores the aligned
+//           16-byte granule that starts inside its window, assembled from
+//           its slot and the copy's next slot, the first slot of a run of
+//           whole slots also stores the bytes before its granule and the
+//           last one the bytes after it (binary32; an unaligned bfloat16
+//           slot is stored element by element).
+// A slot spanning two tensors moves element by element.
+template <int P, typename T, bool UNPACK>
 __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
     constexpr int ES = sizeof(T);
-    constexpr int SB = 4 * ES;  // slot bytes
-    constexpr int B = TC_TP_BATCH;
+    constexpr int SB = 4 * ES;                      // slot bytes
+    constexpr int M = 1024 / P > 16 ? 1024 / P : 16;  // slots per LDS tile
+    constexpr int ROW = (P + 1) * SB;               // padded tile row, bytes
     __shared__ int32_t s_rel[kMaxStage + 1];
-    __shared__ const char* s_ptr[kMaxStage];
-    const int tid = threadIdx.x;
+    __shared__ uintptr_t s_base[kMaxStage];
+    __shared__ __attribute__((aligned(16))) unsigned char s_tile[M * ROW];
+    const int K = a.K;
     const int64_t cstart = static_cast<int64_t>(blockIdx.x) * a.chunk;
     const int32_t clen = static_cast<int32_t>(a.N - cstart < a.chunk ? a.N - cstart : a.chunk);
     const int32_t lo = a.chunk_first[blockIdx.x];
     const int32_t hi = a.chunk_first[blockIdx.x + 1];
     const int nseg = hi - lo + 1;
-    const int K = a.K;
     const int64_t first_start = a.offsets[lo] - cstart;
-    const bool staged = static_cast<int64_t>(nseg) * K <= kMaxStage;  // pointers for all copies fit
     const bool rel_staged = nseg <= kMaxStage;
-    for (int s = tid; s <= nseg && rel_staged; s += 256) s_rel[s] = clamp_rel(a.offsets[lo + s] - cstart, clen);
-    if (staged)
-        for (int q = tid; q < nseg * K; q += 256)
-            s_ptr[q] = static_cast<const char*>(a.ptrs[static_cast<int64_t>(q / nseg) * a.n + lo + q % nseg]);
+    const bool base_staged = static_cast<int64_t>(nseg) * K <= kMaxStage;
+    auto rel_global = [&](int s) -> int32_t { return clamp_rel(a.offsets[lo + s] - cstart, clen); };
+    auto base_global = [&](int kk, int s) -> uintptr_t {
+        const int64_t st = s == 0 ? first_start : a.offsets[lo + s] - cstart;
+        return reinterpret_cast<uintptr_t>(a.ptrs[static_cast<int64_t>(kk) * a.n + lo + s]) -
+               static_cast<uintptr_t>(st * ES);
+    };
+    if (rel_staged)
+        for (int s = threadIdx.x; s <= nseg; s += 256) s_rel[s] = rel_global(s);
+    if (base_staged)
+        for (int q = threadIdx.x; q < nseg * K; q += 256) s_base[q] = base_global(q / nseg, q % nseg);
     __syncthreads();
-    auto rel = [&](int s) -> int32_t {
-        return rel_staged ? s_rel[s] : clamp_rel(a.offsets[lo + s] - cstart, clen);
-    };
-    auto ptr = [&](int k, int s) -> const char* {
-        return staged ? s_ptr[k * nseg + s] : static_cast<const char*>(a.ptrs[static_cast<int64_t>(k) * a.n + lo + s]);
-    };
-    auto start = [&](int s) -> int64_t { return s == 0 ? first_start : rel(s); };
+    auto rel = [&](int s) -> int32_t { return rel_staged ? s_rel[s] : rel_global(s); };
+    auto base = [&](int kk, int s) -> uintptr_t { return base_staged ? s_base[kk * nseg + s] : base_global(kk, s); };
     auto find = [&](int jr) {  // last segment whose start is <= jr
         int l = 0, h = nseg - 1;
         while (l < h) {
@@ -300,64 +372,143 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
         }
         return l;
     };
-    char* tens = static_cast<char*>(a.tensor);
+    const uintptr_t tens = reinterpret_cast<uintptr_t>(a.tensor);
     const int64_t slot0 = cstart / 4;
+    auto piece = [&](int js, int kk) -> uintptr_t {
+        return tens + static_cast<uintptr_t>(((slot0 + js) * K + kk) * SB);
+    };
+    auto tile = [&](int jl, int kk) -> unsigned char* { return s_tile + jl * ROW + kk * SB; };
     const int nsl = clen / 4;  // whole slots in this chunk
-    const int npieces = nsl * K;
-    for (int q0 = tid; q0 < npieces; q0 += 256 * B) {
-        u4 val[B];
-        uintptr_t dst[B];
-        bool vec[B];
+    for (int t0 = 0; t0 < nsl; t0 += M) {
+        const int mt = nsl - t0 < M ? nsl - t0 : M;  // slots in this tile
+        // each phase moves M*P = 1024 pieces: 4 per lane, all loads issued
+        // before the first write
+        constexpr int R = (M * P) / 256;
+        if (!UNPACK) {
+            // copies -> tile: lanes walk consecutive slots of one copy
+            u4 v[R];
+            bool ok[R];
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int q = q0 + b * 256;
-            vec[b] = false;
-            if (q >= npieces) continue;
-            const int js = q / K, k = q - js * K;
-            const int jr = 4 * js;
-            const uintptr_t piece = reinterpret_cast<uintptr_t>(tens) + ((slot0 + js) * K + k) * SB;
-            int s = find(jr);
-            if (jr + 4 <= rel(s + 1)) {
-                const uintptr_t w = reinterpret_cast<uintptr_t>(ptr(k, s)) + (jr - start(s)) * ES;
-                if (!UNPACK) {
-                    val[b] = load_bytes<SB>(w);
-                    dst[b] = piece;
-                    vec[b] = true;
-                } else if ((w & (SB - 1)) == 0) {
-                    val[b] = load_bytes<SB>(piece);
-                    dst[b] = w;
-                    vec[b] = true;
-                } else {
-                    const T* src = reinterpret_cast<const T*>(piece);
-                    T* d = reinterpret_cast<T*>(w);
+            for (int r = 0; r < R; ++r) {
+                const int q = threadIdx.x + r * 256;
+                const int kk = q / M, jl = q % M;
+                ok[r] = kk < K && jl < mt;
+                if (!ok[r]) continue;
+                const int js = t0 + jl, jr = 4 * js;
+                int s = find(jr);
+                if (jr + 4 <= rel(s + 1)) {
+                    v[r] = load_bytes<SB>(base(kk, s) + static_cast<uintptr_t>(jr) * ES);
+                } else {  // the slot spans tensors
+                    T e4[4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) d[e] = src[e];
+                    for (int e = 0; e < 4; ++e) {
+                        while (jr + e >= rel(s + 1)) ++s;
+                        e4[e] = reinterpret_cast<const T*>(base(kk, s))[jr + e];
+                    }
+                    v[r] = u4{0u, 0u, 0u, 0u};
+                    __builtin_memcpy(&v[r], e4, SB);
                 }
-            } else {  // the slot's 4 elements span tensors
-                T* pc = reinterpret_cast<T*>(piece);
+            }
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int je = jr + e;
-                    while (je >= rel(s + 1)) ++s;
-                    T* t = reinterpret_cast<T*>(const_cast<char*>(ptr(k, s))) + (je - start(s));
-                    if (UNPACK) *t = pc[e];
-                    else pc[e] = *t;
+            for (int r = 0; r < R; ++r) {
+                if (!ok[r]) continue;
+                const int q = threadIdx.x + r * 256;
+                if constexpr (SB == 16) *reinterpret_cast<u4*>(tile(q % M, q / M)) = v[r];
+                else *reinterpret_cast<u2*>(tile(q % M, q / M)) = u2{v[r].x, v[r].y};
+            }
+            __syncthreads();
+            // tile -> tensor, in tensor order
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int q = threadIdx.x + r * 256;
+                const int jl = q / P, kk = q % P;
+                if (kk >= K || jl >= mt) continue;
+                if constexpr (SB == 16)
+                    __builtin_nontemporal_store(*reinterpret_cast<const u4*>(tile(jl, kk)),
+                                                reinterpret_cast<u4*>(piece(t0 + jl, kk)));
+                else
+                    __builtin_nontemporal_store(*reinterpret_cast<const u2*>(tile(jl, kk)),
+                                                reinterpret_cast<u2*>(piece(t0 + jl, kk)));
+            }
+        } else {
+            // tensor -> tile, in tensor order
+            u4 v[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int q = threadIdx.x + r * 256;
+                const int jl = q / P, kk = q % P;
+                if (kk >= K || jl >= mt) continue;
+                if constexpr (SB == 16) {
+                    v[r] = __builtin_nontemporal_load(reinterpret_cast<const u4*>(piece(t0 + jl, kk)));
+                } else {
+                    const u2 w = __builtin_nontemporal_load(reinterpret_cast<const u2*>(piece(t0 + jl, kk)));
+                    v[r] = u4{w.x, w.y, 0u, 0u};
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int q = threadIdx.x + r * 256;
+                const int jl = q / P, kk = q % P;
+                if (kk >= K || jl >= mt) continue;
+                if constexpr (SB == 16) *reinterpret_cast<u4*>(tile(jl, kk)) = v[r];
+                else *reinterpret_cast<u2*>(tile(jl, kk)) = u2{v[r].x, v[r].y};
+            }
+            __syncthreads();
+            // tile -> copies: lanes walk consecutive slots of one copy
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int q = threadIdx.x + r * 256;
+                const int kk = q / M, jl = q % M;
+                if (kk >= K || jl >= mt) continue;
+                const int js = t0 + jl, jr = 4 * js;
+                int s = find(jr);
+                const int32_t r1 = rel(s + 1);
+                const T* src = reinterpret_cast<const T*>(tile(jl, kk));
+                if (jr + 4 <= r1) {
+                    const uintptr_t w = base(kk, s) + static_cast<uintptr_t>(jr) * ES;
+                    if ((w & (SB - 1)) == 0) {
+                        if constexpr (SB == 16)
+                            __builtin_nontemporal_store(*reinterpret_cast<const u4*>(src), reinterpret_cast<u4*>(w));
+                        else
+                            __builtin_nontemporal_store(*reinterpret_cast<const u2*>(src), reinterpret_cast<u2*>(w));
+                    } else if constexpr (SB == 16) {
+                        const uintptr_t G = (w + 15) & ~uintptr_t(15);
+                        const uint32_t sh = static_cast<uint32_t>(G - w);  // bytes of this slot before G
+                        const int run_lo = (rel(s) + 3) / 4, run_hi = r1 / 4;  // whole slots of this tensor here
+                        if (js == run_lo)  // bytes before the first granule
+                            for (uint32_t e = 0; e < sh / ES; ++e) reinterpret_cast<T*>(w)[e] = src[e];
+                        if (js + 1 < run_hi) {
+                            const u4 next = jl + 1 < mt ? *reinterpret_cast<const u4*>(tile(jl + 1, kk))
+                                                        : load_bytes<SB>(piece(js + 1, kk));
+                            __builtin_nontemporal_store(funnel(*reinterpret_cast<const u4*>(src), next, sh),
+                                                        reinterpret_cast<u4*>(G));
+                        } else {  // the last whole slot: bytes after G
+                            for (uint32_t e = sh / ES; e < 4; ++e) reinterpret_cast<T*>(w)[e] = src[e];
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) reinterpret_cast<T*>(w)[e] = src[e];
+                    }
+                } else {  // the slot spans tensors
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        while (jr + e >= rel(s + 1)) ++s;
+                        reinterpret_cast<T*>(base(kk, s))[jr + e] = src[e];
+                    }
                 }
             }
         }
-#pragma unroll
-        for (int b = 0; b < B; ++b)
-            if (vec[b]) store_bytes<SB>(dst[b], val[b]);
+        __syncthreads();  // the tile is reused
     }
     // the group's last, partial slot: element by element, every copy
     const int rem = clen - 4 * nsl;
-    if (tid < rem * K) {
-        const int k = tid / rem, e = tid - k * rem;
+    if (threadIdx.x < rem * K) {
+        const int kk = threadIdx.x / rem, e = threadIdx.x - kk * rem;
         const int je = 4 * nsl + e;
         int s = find(je);
         while (je >= rel(s + 1)) ++s;
-        T* t = reinterpret_cast<T*>(const_cast<char*>(ptr(k, s))) + (je - start(s));
-        T* pc = reinterpret_cast<T*>(tens) + ((slot0 + nsl) * K + k) * 4 + e;
+        T* t = reinterpret_cast<T*>(base(kk, s)) + je;
+        T* pc = reinterpret_cast<T*>(tens) + ((slot0 + nsl) * K + kk) * 4 + e;
         if (UNPACK) *t = *pc;
         else *pc = *t;
     }
@@ -365,13 +516,17 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
 
 // ---------------------------------------------------------- launching
 
-// Slots per lane: two for the reduction, one for the step (measured).
-constexpr int kTReduceUnroll = 2;
-constexpr int kTEasgdUnroll = 1;
+// Slots per lane: enough that a wave's single-stream output covers a
+// 128-byte line (P/8 for P >= 16); the reduction takes at least 2, the
+// step 1 (measured).
+// bfloat16 inputs (8-byte slots) take twice the slots to keep as many
+// bytes in flight.
+constexpr int treduce_unroll(int P, int es) { return (P / 8 > 2 ? P / 8 : 2) * (4 / es); }
+constexpr int teasgd_unroll(int P) { return P / 8 > 1 ? P / 8 : 1; }
 
 template <int P, typename T>
 hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hipStream_t s) {
-    constexpr int U = kTReduceUnroll;
+    constexpr int U = treduce_unroll(P, sizeof(T));
     constexpr int SPB = 256 / P;
     TReduceArgs<T> a{static_cast<const T*>(in), out, n / 4, n, K, op};
     const int64_t blocks = (a.nslot + SPB * U - 1) / (SPB * U);
@@ -385,7 +540,7 @@ hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hip
 
 template <int P, typename T>
 hipError_t run_teasgd(int K, float* x, const void* g, float* xc, float eta, float rho, int64_t n, hipStream_t s) {
-    constexpr int U = kTEasgdUnroll;
+    constexpr int U = teasgd_unroll(P);
     constexpr int SPB = 256 / P;
     TEasgdArgs<T> a{x, static_cast<const T*>(g), xc, n / 4, n, eta, rho, eta * rho, K};
     const int64_t blocks = (a.nslot + SPB * U - 1) / (SPB * U);
@@ -436,18 +591,30 @@ hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, floa
     return dispatch_teasgd<float>(K, x, g, xc, eta, rho, n, stream);
 }
 
+template <int P>
+hipError_t run_tpack(const TPackArgs& a, int elem, bool unpack, unsigned blocks, hipStream_t stream) {
+    dim3 grid(blocks);
+    if (elem == 2) {
+        if (unpack) hipLaunchKernelGGL((tensor_pack_kernel<P, uint16_t, true>), grid, dim3(256), 0, stream, a);
+        else hipLaunchKernelGGL((tensor_pack_kernel<P, uint16_t, false>), grid, dim3(256), 0, stream, a);
+    } else {
+        if (unpack) hipLaunchKernelGGL((tensor_pack_kernel<P, uint32_t, true>), grid, dim3(256), 0, stream, a);
+        else hipLaunchKernelGGL((tensor_pack_kernel<P, uint32_t, false>), grid, dim3(256), 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStream_t stream) {
     const tc_group* g = tl->g;
     TPackArgs a{g->d_offsets, g->d_chunk_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, g->chunk};
-    dim3 grid(static_cast<unsigned>(g->nchunks));
-    if (tl->elem == 2) {
-        if (unpack) hipLaunchKernelGGL((tensor_pack_kernel<uint16_t, true>), grid, dim3(256), 0, stream, a);
-        else hipLaunchKernelGGL((tensor_pack_kernel<uint16_t, false>), grid, dim3(256), 0, stream, a);
-    } else {
-        if (unpack) hipLaunchKernelGGL((tensor_pack_kernel<uint32_t, true>), grid, dim3(256), 0, stream, a);
-        else hipLaunchKernelGGL((tensor_pack_kernel<uint32_t, false>), grid, dim3(256), 0, stream, a);
+    const unsigned blocks = static_cast<unsigned>(g->nchunks);
+    switch (next_pow2(tl->K)) {
+#define TC_CASE(p) \
+    case p: return run_tpack<p>(a, tl->elem, unpack, blocks, stream);
+        TC_FOR_P(TC_CASE)
+#undef TC_CASE
+        default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 }  // namespace tc
