@@ -64,6 +64,19 @@ class Oracle:
                                           ctypes.POINTER(_VP), ctypes.c_int32, _DP,
                                           ctypes.c_double, ctypes.c_double]
         lib.oracle_easgd_step.restype = None
+        lib.oracle_sgd_step.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(_DP),
+                                        ctypes.POINTER(_VP), ctypes.c_int32, ctypes.c_double]
+        lib.oracle_sgd_step.restype = None
+        lib.oracle_elastic_async.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(_DP), _DP,
+                                             ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_double]
+        lib.oracle_elastic_async.restype = None
+        lib.oracle_sync_sgd.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(_DP),
+                                        ctypes.POINTER(_VP), ctypes.c_int32, ctypes.c_double,
+                                        ctypes.c_double, _DP]
+        lib.oracle_sync_sgd.restype = None
+        lib.oracle_broadcast.argtypes = [ctypes.c_int32, ctypes.c_int64, _VP, ctypes.c_int32,
+                                         ctypes.POINTER(_VP)]
+        lib.oracle_broadcast.restype = None
         lib.oracle_tensor_from_copies.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(_VP),
                                                   ctypes.c_int32, _VP]
         lib.oracle_tensor_from_copies.restype = None
@@ -145,6 +158,41 @@ class Oracle:
             self.lib.oracle_easgd_step(K, n, xp, gp, self._dtype_code(gs[0]),
                                        xc.ctypes.data_as(_DP), float(eta), float(rho))
 
+
+    # -- schedules and synchronous SGD ---------------------------------------
+    @staticmethod
+    def _state_ptrs(xs):
+        for a in xs:
+            assert a.dtype == np.float64 and a.flags.c_contiguous
+        return (_DP * len(xs))(*[a.ctypes.data_as(_DP) for a in xs])
+
+    def sgd_step(self, xs: Sequence[np.ndarray], gs: Sequence[np.ndarray], eta: float) -> None:
+        """x_i -= eta * g_i in place (binary64 state, stored gradients)."""
+        gs = [np.ascontiguousarray(a) for a in gs]
+        self.lib.oracle_sgd_step(len(xs), xs[0].size, self._state_ptrs(xs), self._ptrs(gs),
+                                 self._dtype_code(gs[0]), float(eta))
+
+    def elastic_async(self, xs: Sequence[np.ndarray], xc: np.ndarray, order: Sequence[int], alpha: float) -> None:
+        """Per-worker elastic exchanges in the given order, in place."""
+        assert xc.dtype == np.float64 and xc.flags.c_contiguous
+        o = np.ascontiguousarray(np.asarray(order, dtype=np.int32))
+        assert len(o) == 0 or (o.min() >= 0 and o.max() < len(xs))
+        self.lib.oracle_elastic_async(len(xs), xc.size, self._state_ptrs(xs), xc.ctypes.data_as(_DP),
+                                      o.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), len(o), float(alpha))
+
+    def sync_sgd(self, xs: Sequence[np.ndarray], gs: Sequence[np.ndarray], eta: float, rescale: float):
+        """x_i -= eta * rescale * sum_j g_j in place; returns the sum."""
+        gs = [np.ascontiguousarray(a) for a in gs]
+        out = np.empty(xs[0].size, dtype=np.float64)
+        self.lib.oracle_sync_sgd(len(xs), xs[0].size, self._state_ptrs(xs), self._ptrs(gs),
+                                 self._dtype_code(gs[0]), float(eta), float(rescale), out.ctypes.data_as(_DP))
+        return out
+
+    def broadcast(self, src: np.ndarray, K: int) -> List[np.ndarray]:
+        src = np.ascontiguousarray(src)
+        outs = [np.empty_like(src) for _ in range(K)]
+        self.lib.oracle_broadcast(K, src.size, src.ctypes.data, src.dtype.itemsize, self._ptrs(outs))
+        return outs
 
     # -- tensor layout ------------------------------------------------------
     @staticmethod

@@ -24,6 +24,20 @@
  *                   locally computed gradients; Sec. 3.2: push first sums
  *                   the tensors of one key; Sec. 5 (synchronous SGD): the
  *                   sum is rescaled by 1/mini_batch_size, i.e. averaged.
+ *   sgd step        Sec. 2.1, Eq. (1) with dw = -eta * g; Sec. 5 listings:
+ *                   SGD.Update(params, grads, rescale) scales the step by
+ *                   rescale, folded here into eta.
+ *   async exchange  Sec. 2.2, Eqs. (2) and (3) for one worker at a time:
+ *                   the asynchronous elastic averaging of the ESGD listing
+ *                   (Sec. 5), where each worker's push updates the center
+ *                   (Elastic1) and the worker moves toward the center
+ *                   (Elastic2), workers in arrival order.
+ *   sync pushpull   Sec. 5, synchronous SGD: push and pull (or pushpull,
+ *                   Sec. 3.2) leave every worker's gradient equal to the sum
+ *                   over the workers; SGD.Update then applies it with rescale
+ *                   1/mini_batch_size.
+ *   broadcast       Sec. 3.2: pull copies one value to every tensor of the
+ *                   list.
  *   tensor layout   Sec. 6.1: a "tensor" is a grouping of vectors, one from
  *                   each worker, handled as one unit.  Here the K copies
  *                   are held in one buffer, interleaved in slots of four
@@ -208,4 +222,65 @@ void oracle_copies_from_tensor(int32_t K, int64_t N, const void* tensor,
             memcpy((unsigned char*)copies[i] + e * elem_bytes,
                    src + tensor_index(K, e, i) * elem_bytes,
                    (size_t)elem_bytes);
+}
+
+/*
+ * Plain SGD on K workers, in place: x[i][j] = x_i - eta * g_i.
+ */
+void oracle_sgd_step(int32_t K, int64_t N, double* const* x, const void* const* g,
+                     int32_t g_dtype, double eta)
+{
+    for (int32_t i = 0; i < K; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            x[i][j] = x[i][j] - eta * stored_value(g[i], g_dtype, j);
+}
+
+/*
+ * Asynchronous elastic exchanges, in place: for each worker w = order[r],
+ * r = 0 .. R-1 in turn, with d = x_w - c taken from the values before this
+ * exchange,
+ *   center:  c   = c + alpha * d      (Elastic1, on the server)
+ *   worker:  x_w = x_w - alpha * d    (Elastic2, on the client)
+ * so each later exchange sees the center left by the earlier ones.
+ */
+void oracle_elastic_async(int32_t K, int64_t N, double* const* x, double* xc,
+                          const int32_t* order, int32_t R, double alpha)
+{
+    (void)K;
+    for (int64_t j = 0; j < N; ++j)
+        for (int32_t r = 0; r < R; ++r) {
+            int32_t w = order[r];
+            double d = x[w][j] - xc[j];
+            xc[j] = xc[j] + alpha * d;
+            x[w][j] = x[w][j] - alpha * d;
+        }
+}
+
+/*
+ * Synchronous SGD through pushpull: with S_j = g_0[j] + ... + g_{K-1}[j]
+ * (the value push/pull leave in every worker's gradient),
+ *   x[i][j] = x_i - eta * rescale * S_j    for every worker i,
+ * and, when broadcast is set, every g_i[j] becomes S_j (returned in the
+ * binary64 array sum_out, which the caller compares with each copy).
+ */
+void oracle_sync_sgd(int32_t K, int64_t N, double* const* x, const void* const* g,
+                     int32_t g_dtype, double eta, double rescale, double* sum_out)
+{
+    for (int64_t j = 0; j < N; ++j) {
+        double S = 0.0;
+        for (int32_t i = 0; i < K; ++i)
+            S += stored_value(g[i], g_dtype, j);
+        for (int32_t i = 0; i < K; ++i)
+            x[i][j] = x[i][j] - eta * rescale * S;
+        if (sum_out)
+            sum_out[j] = S;
+    }
+}
+
+/* Broadcast: dst_i[j] = src[j] for every copy i, bit for bit. */
+void oracle_broadcast(int32_t K, int64_t N, const void* src, int32_t elem_bytes,
+                      void* const* dst)
+{
+    for (int32_t i = 0; i < K; ++i)
+        memcpy(dst[i], src, (size_t)(N * elem_bytes));
 }

@@ -355,6 +355,94 @@ def pin_easgd_bf16_equals_widened(orc):
     assert all(np.array_equal(a, b) for a, b in zip(xs, xa)) and np.array_equal(xc, ca)
 
 
+# ------------------------------------------------- schedules and sync SGD
+
+def pin_sgd_step_is_textbook(orc):
+    """sgd_step is w - eta*g per worker (Sec. 2.1, Eq. 1), and equals the
+    elastic step with rho = 0 on the workers."""
+    rng = _rng(20)
+    K = 5
+    xs, xc, gs = _state(rng, K, 300)
+    x0 = [x.copy() for x in xs]
+    orc.sgd_step(xs, gs, 0.05)
+    for x, x_old, g in zip(xs, x0, gs):
+        assert np.array_equal(x, x_old - 0.05 * g.astype(np.float64))
+    xe = [x.copy() for x in x0]
+    orc.easgd_step(xe, gs, xc.copy(), 0.05, 0.0)
+    assert all(np.array_equal(a, b) for a, b in zip(xs, xe))
+
+
+def pin_elastic_async_conserves_pairs(orc):
+    """Each exchange moves worker and center by equal and opposite amounts:
+    sum_i x_i + x_c is invariant; the exchanged worker's gap to the center
+    shrinks by (1 - 2 alpha)."""
+    rng = _rng(21)
+    K, alpha = 6, 0.1
+    xs, xc, _ = _state(rng, K, 400)
+    before = sum(xs) + xc
+    mag = sum(np.abs(x) for x in xs) + np.abs(xc)
+    order = [3, 0, 5, 3, 1]
+    orc.elastic_async(xs, xc, order, alpha)
+    assert _close(sum(xs) + xc, before, 1e-13, mag)
+    # a single exchange, checked in closed form
+    xs2, xc2, _ = _state(rng, K, 400)
+    gap = xs2[2] - xc2
+    x2, c2 = xs2[2].copy(), xc2.copy()
+    orc.elastic_async(xs2, xc2, [2], alpha)
+    assert _close(xs2[2] - xc2, (1 - 2 * alpha) * gap, 1e-13, np.abs(x2) + np.abs(c2))
+    assert _close(xc2, c2 + alpha * gap, 1e-13, np.abs(x2) + np.abs(c2))
+
+
+def pin_elastic_async_is_sequential(orc):
+    """Exchanges see the center left by the earlier ones: two exchanges of
+    the same worker equal the single-exchange map applied twice, and an
+    empty order changes nothing."""
+    rng = _rng(22)
+    xs, xc, _ = _state(rng, 3, 200)
+    xa, ca = [x.copy() for x in xs], xc.copy()
+    orc.elastic_async(xa, ca, [1, 1], 0.2)
+    xb, cb = [x.copy() for x in xs], xc.copy()
+    orc.elastic_async(xb, cb, [1], 0.2)
+    orc.elastic_async(xb, cb, [1], 0.2)
+    assert all(np.array_equal(a, b) for a, b in zip(xa, xb)) and np.array_equal(ca, cb)
+    xe, ce = [x.copy() for x in xs], xc.copy()
+    orc.elastic_async(xe, ce, [], 0.2)
+    assert all(np.array_equal(a, b) for a, b in zip(xe, xs)) and np.array_equal(ce, xc)
+    # order matters once two different workers exchange
+    xo, co = [x.copy() for x in xs], xc.copy()
+    orc.elastic_async(xo, co, [2, 1], 0.2)
+    assert not np.allclose(co, ca)
+
+
+def pin_sync_sgd_identical_steps(orc):
+    """Synchronous SGD: every worker takes the same step -eta*rescale*S with
+    S the reduce-SUM of the gradients; identical workers stay identical;
+    with rescale = 1/K it is SGD with the average gradient."""
+    rng = _rng(23)
+    K = 4
+    x = rng.normal(0, 0.05, 300)
+    xs = [x.copy() for _ in range(K)]
+    gs = [rng.normal(0, 0.01, 300).astype(np.float32) for _ in range(K)]
+    S = orc.sync_sgd(xs, gs, 0.05, 1.0 / K)
+    assert np.array_equal(S, orc.reduce(gs, 0))
+    assert all(np.array_equal(a, xs[0]) for a in xs)
+    avg = orc.reduce(gs, 1)
+    assert _close(xs[0], x - 0.05 * avg, 1e-14, np.abs(x) + 0.05 * np.abs(avg))
+    # integer gradients: exact
+    gi = [rng.integers(-100, 101, 300).astype(np.float32) for _ in range(K)]
+    xi = [np.zeros(300) for _ in range(K)]
+    S = orc.sync_sgd(xi, gi, 1.0, 1.0)
+    assert np.array_equal(xi[1], -np.sum(np.stack([g.astype(np.int64) for g in gi]), axis=0).astype(np.float64))
+
+
+def pin_broadcast_copies(orc):
+    rng = _rng(24)
+    for dtype in (np.float32, np.uint16):
+        src = _tensors(rng, [77], dtype)[0]
+        outs = orc.broadcast(src, 5)
+        assert len(outs) == 5 and all(np.array_equal(o.view(np.uint8), src.view(np.uint8)) for o in outs)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]
 
 

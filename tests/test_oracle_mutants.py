@@ -53,6 +53,17 @@ MUTANTS = [
      "double gi = stored_value(g[K - 1 - i], g_dtype, j);"),
     ("tensor_slot_width", "return ((e / 4) * K + i) * 4 + (e % 4);", "return ((e / 2) * K + i) * 2 + (e % 2);"),
     ("tensor_worker_major", "return ((e / 4) * K + i) * 4 + (e % 4);", "return (i * ((e / 4) + 1) + (e / 4)) * 4 + (e % 4);"),
+    ("sgd_sign", "x[i][j] = x[i][j] - eta * stored_value(g[i], g_dtype, j);",
+     "x[i][j] = x[i][j] + eta * stored_value(g[i], g_dtype, j);"),
+    ("async_center_sign", "xc[j] = xc[j] + alpha * d;", "xc[j] = xc[j] - alpha * d;"),
+    ("async_worker_reads_new_center", "x[w][j] = x[w][j] - alpha * d;",
+     "x[w][j] = x[w][j] - alpha * (x[w][j] - xc[j]);"),
+    ("async_ignores_order", "int32_t w = order[r];", "int32_t w = r % K;"),
+    ("sync_sgd_drops_rescale", "x[i][j] = x[i][j] - eta * rescale * S;", "x[i][j] = x[i][j] - eta * S;"),
+    ("sync_sgd_own_gradient", "x[i][j] = x[i][j] - eta * rescale * S;",
+     "x[i][j] = x[i][j] - eta * rescale * K * stored_value(g[i], g_dtype, j);"),
+    ("broadcast_short", "memcpy(dst[i], src, (size_t)(N * elem_bytes));",
+     "memcpy(dst[i], src, (size_t)((N - (N > 1)) * elem_bytes));"),
     ("center_reads_new_workers",
      "        for (int32_t i = 0; i < K; ++i)\n            spread += x[i][j] - c;\n",
      ""),
