@@ -231,6 +231,91 @@ int32_t tc_reduce_tensor(const tc_group* g, int32_t K, const void* in, int32_t i
 int32_t easgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad,
                           int32_t g_dtype, float* x_c, float eta, float rho, void* stream);
 
+/* ------------------------------------------------------------------------
+ * The ESGD schedule with a communication period (Sec. 5, the ESGD listing:
+ * SGD.Update every iteration, the elastic exchange every INTERVAL = 64
+ * iterations) and its pieces.
+ *
+ * sgd_step: plain SGD on every worker, in place (Sec. 2.1, Eq. 1, dw =
+ * -eta g; SGD.Update's rescale folded into eta):
+ *     x[i][j] = fma(-eta, grad[i][j], x[i][j]).
+ * x: K device pointers to N binary32 values, pairwise disjoint; grad: K
+ * device pointers to N values of g_dtype, not overlapping any x.
+ * ---------------------------------------------------------------------- */
+int32_t sgd_step(const tc_group* g, int32_t K, float* const* x, const void* const* grad,
+                 int32_t g_dtype, float eta, void* stream);
+
+/* sgd_step on tensor-layout workers and gradients (16-byte aligned,
+ * disjoint). */
+int32_t sgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad,
+                        int32_t g_dtype, float eta, void* stream);
+
+/* One iteration of the periodic schedule: easgd_step_ex when
+ * iteration % tau == 0, else sgd_step (x_c untouched).  tau >= 1,
+ * iteration >= 0; arguments as for those two calls. */
+int32_t easgd_period_step(const tc_group* g, int32_t K, float* const* x,
+                          const void* const* grad, int32_t g_dtype, float* x_c, float eta,
+                          float rho, int64_t iteration, int32_t tau, void* stream);
+
+/* The same on the tensor layout (easgd_step_tensor / sgd_step_tensor). */
+int32_t easgd_period_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad,
+                                 int32_t g_dtype, float* x_c, float eta, float rho,
+                                 int64_t iteration, int32_t tau, void* stream);
+
+/* ------------------------------------------------------------------------
+ * elastic_async: asynchronous elastic averaging, one worker at a time
+ * (Sec. 2.2, Eqs. 2 and 3; Sec. 5, the asynchronous ESGD listing: a
+ * worker's push makes the server apply Elastic1 to the center and the
+ * worker applies Elastic2).  For r = 0 .. R-1 in turn, with w = order[r]
+ * and d = x_w - c from the values before this exchange:
+ *     c   = fma(alpha, d, c)          (the center moves toward the worker)
+ *     x_w = fma(-alpha, d, x_w)       (the worker moves toward the center)
+ * so later exchanges see the center left by earlier ones; each exchange
+ * leaves x_w + c unchanged in exact arithmetic.  order: host array of R
+ * worker indices in [0, K), no worker twice (0 <= R <= K; R = 0 is a
+ * no-op); alpha finite.  x: K disjoint binary32 buffers; x_c: N binary32
+ * values not overlapping them.
+ * ---------------------------------------------------------------------- */
+int32_t elastic_async(const tc_group* g, int32_t K, float* const* x, float* x_c,
+                      const int32_t* order, int32_t R, float alpha, void* stream);
+
+/* elastic_async on tensor-layout workers (16-byte aligned x and x_c). */
+int32_t elastic_async_tensor(const tc_group* g, int32_t K, float* x, float* x_c,
+                             const int32_t* order, int32_t R, float alpha, void* stream);
+
+/* ------------------------------------------------------------------------
+ * sync_sgd_step: synchronous SGD through pushpull (Sec. 5, the synchronous
+ * SGD listing; Sec. 3.2, pushpull): with S = the pairwise sum of the K
+ * gradients (the value push and pull leave in every worker's gradient),
+ *     x[i][j] = fma(-(eta*rescale), S[j], x[i][j])   for every worker i,
+ * eta*rescale rounded once to binary32 (rescale = 1/mini_batch_size
+ * averages).  With broadcast != 0, every grad[i] is overwritten with S (the
+ * pull's copy to every tensor); binary32 gradients only (TC_EUNSUPPORTED
+ * for bfloat16).  x: K disjoint binary32 buffers; grad: K buffers of
+ * g_dtype not overlapping x (and pairwise disjoint when broadcast).
+ * ---------------------------------------------------------------------- */
+int32_t sync_sgd_step(const tc_group* g, int32_t K, float* const* x, void* const* grad,
+                      int32_t g_dtype, float eta, float rescale, int32_t broadcast, void* stream);
+
+/* sync_sgd_step on tensor-layout workers and gradients. */
+int32_t sync_sgd_step_tensor(const tc_group* g, int32_t K, float* x, void* grad,
+                             int32_t g_dtype, float eta, float rescale, int32_t broadcast,
+                             void* stream);
+
+/* ------------------------------------------------------------------------
+ * tc_broadcast: dst[i][j] = src[j] for every copy i < K, bit for bit (the
+ * pull copies the value to every tensor of the list, Sec. 3.2; the tensor
+ * broadcast of Sec. 6.3.1).  src: N elements of dtype; dst: K disjoint
+ * buffers of N elements, not overlapping src.
+ * ---------------------------------------------------------------------- */
+int32_t tc_broadcast(const tc_group* g, int32_t K, const void* src, void* const* dst,
+                     int32_t dtype, void* stream);
+
+/* tc_broadcast into every copy of one tensor-layout buffer (16-byte
+ * aligned src and dst). */
+int32_t tc_broadcast_tensor(const tc_group* g, int32_t K, const void* src, void* dst,
+                            int32_t dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -13,6 +13,13 @@ loading fails loudly when the library has not been built.
     reduce(g, ins, out, "avg")              # tc_reduce / tc_reduce_ex
     easgd_step(g, xs, gs, xc, eta, rho)     # easgd_step / easgd_step_ex
 
+Schedules and synchronous SGD (separate buffers; *_tensor on the tensor layout):
+    sgd_step(g, xs, gs, eta)                # sgd_step
+    easgd_period_step(g, xs, gs, xc, eta, rho, t, tau)  # easgd_period_step
+    elastic_async(g, xs, xc, order, alpha)  # elastic_async
+    sync_sgd_step(g, xs, gs, eta, rescale, broadcast)   # sync_sgd_step
+    broadcast(g, src, dsts)                 # tc_broadcast
+
 Tensor layout (the K copies interleaved in one buffer):
     n = tensor_numel(g, K)                  # tc_tensor_numel
     pack_tensor(tl, T); unpack_tensor(tl, T)            # tc_pack_tensor / tc_unpack_tensor
@@ -83,6 +90,16 @@ def lib(path: str = LIBRARY) -> ctypes.CDLL:
         "tc_unpack_tensor": (i32, [_VP, _VP, _VP]),
         "tc_reduce_tensor": (i32, [_VP, i32, _VP, i32, _VP, i32, _VP]),
         "easgd_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, _VP, f32, f32, _VP]),
+        "sgd_step": (i32, [_VP, i32, _VPP, _VPP, i32, f32, _VP]),
+        "sgd_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, f32, _VP]),
+        "easgd_period_step": (i32, [_VP, i32, _VPP, _VPP, i32, _VP, f32, f32, i64, i32, _VP]),
+        "easgd_period_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, _VP, f32, f32, i64, i32, _VP]),
+        "elastic_async": (i32, [_VP, i32, _VPP, _VP, ctypes.POINTER(i32), i32, f32, _VP]),
+        "elastic_async_tensor": (i32, [_VP, i32, _VP, _VP, ctypes.POINTER(i32), i32, f32, _VP]),
+        "sync_sgd_step": (i32, [_VP, i32, _VPP, _VPP, i32, f32, f32, i32, _VP]),
+        "sync_sgd_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, f32, f32, i32, _VP]),
+        "tc_broadcast": (i32, [_VP, i32, _VP, _VPP, i32, _VP]),
+        "tc_broadcast_tensor": (i32, [_VP, i32, _VP, _VP, i32, _VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -275,3 +292,104 @@ def easgd_step_tensor(group: Group, K: int, x: torch.Tensor, g: torch.Tensor, xc
                                    _dev_ptr(g, n, (gdt,), "grad"), _DTYPES[gdt],
                                    _dev_ptr(xc, group.numel, (torch.float32,), "x_c"), float(eta), float(rho),
                                    _stream(stream)))
+
+
+# ----------------------------------------------- schedules and synchronous SGD
+
+def _gdt(gs_or_g) -> torch.dtype:
+    dt = gs_or_g[0].dtype if isinstance(gs_or_g, (list, tuple)) else gs_or_g.dtype
+    if dt not in _DTYPES:
+        raise TypeError(f"gradients have dtype {dt}")
+    return dt
+
+
+def _workers(group: Group, xs):
+    return _ptr_array([_dev_ptr(t, group.numel, (torch.float32,), f"x[{i}]") for i, t in enumerate(xs)])
+
+
+def _grads(group: Group, gs, dt):
+    return _ptr_array([_dev_ptr(t, group.numel, (dt,), f"grad[{i}]") for i, t in enumerate(gs)])
+
+
+def sgd_step(group: Group, xs, gs, eta: float, stream=None) -> None:
+    """x_i -= eta * g_i for every worker, in place (sgd_step)."""
+    dt = _gdt(gs)
+    _check(lib().sgd_step(group.handle, len(xs), _workers(group, xs), _grads(group, gs, dt), _DTYPES[dt],
+                          float(eta), _stream(stream)))
+
+
+def sgd_step_tensor(group: Group, K: int, x, g, eta: float, stream=None) -> None:
+    dt = _gdt(g)
+    n = tensor_numel(group, K)
+    _check(lib().sgd_step_tensor(group.handle, K, _dev_ptr(x, n, (torch.float32,), "x"), _dev_ptr(g, n, (dt,), "grad"),
+                                 _DTYPES[dt], float(eta), _stream(stream)))
+
+
+def easgd_period_step(group: Group, xs, gs, xc, eta: float, rho: float, iteration: int, tau: int, stream=None) -> None:
+    """The elastic step when iteration % tau == 0, plain SGD otherwise."""
+    dt = _gdt(gs)
+    _check(lib().easgd_period_step(group.handle, len(xs), _workers(group, xs), _grads(group, gs, dt), _DTYPES[dt],
+                                   _dev_ptr(xc, group.numel, (torch.float32,), "x_c"), float(eta), float(rho),
+                                   int(iteration), int(tau), _stream(stream)))
+
+
+def easgd_period_step_tensor(group: Group, K: int, x, g, xc, eta: float, rho: float, iteration: int, tau: int,
+                             stream=None) -> None:
+    dt = _gdt(g)
+    n = tensor_numel(group, K)
+    _check(lib().easgd_period_step_tensor(group.handle, K, _dev_ptr(x, n, (torch.float32,), "x"),
+                                          _dev_ptr(g, n, (dt,), "grad"), _DTYPES[dt],
+                                          _dev_ptr(xc, group.numel, (torch.float32,), "x_c"), float(eta), float(rho),
+                                          int(iteration), int(tau), _stream(stream)))
+
+
+def _order(order):
+    o = [int(v) for v in order]
+    return (ctypes.c_int32 * max(1, len(o)))(*o), len(o)
+
+
+def elastic_async(group: Group, xs, xc, order, alpha: float, stream=None) -> None:
+    """Elastic exchanges of the workers in `order`, one at a time (elastic_async)."""
+    arr, R = _order(order)
+    _check(lib().elastic_async(group.handle, len(xs), _workers(group, xs),
+                               _dev_ptr(xc, group.numel, (torch.float32,), "x_c"), arr, R, float(alpha),
+                               _stream(stream)))
+
+
+def elastic_async_tensor(group: Group, K: int, x, xc, order, alpha: float, stream=None) -> None:
+    arr, R = _order(order)
+    n = tensor_numel(group, K)
+    _check(lib().elastic_async_tensor(group.handle, K, _dev_ptr(x, n, (torch.float32,), "x"),
+                                      _dev_ptr(xc, group.numel, (torch.float32,), "x_c"), arr, R, float(alpha),
+                                      _stream(stream)))
+
+
+def sync_sgd_step(group: Group, xs, gs, eta: float, rescale: float, broadcast: bool = False, stream=None) -> None:
+    """Synchronous SGD through pushpull (sync_sgd_step)."""
+    dt = _gdt(gs)
+    _check(lib().sync_sgd_step(group.handle, len(xs), _workers(group, xs), _grads(group, gs, dt), _DTYPES[dt],
+                               float(eta), float(rescale), int(bool(broadcast)), _stream(stream)))
+
+
+def sync_sgd_step_tensor(group: Group, K: int, x, g, eta: float, rescale: float, broadcast: bool = False,
+                         stream=None) -> None:
+    dt = _gdt(g)
+    n = tensor_numel(group, K)
+    _check(lib().sync_sgd_step_tensor(group.handle, K, _dev_ptr(x, n, (torch.float32,), "x"),
+                                      _dev_ptr(g, n, (dt,), "grad"), _DTYPES[dt], float(eta), float(rescale),
+                                      int(bool(broadcast)), _stream(stream)))
+
+
+def broadcast(group: Group, src, dsts, stream=None) -> None:
+    """dsts[i] = src for every copy (tc_broadcast)."""
+    dt = _gdt(src)
+    p = _ptr_array([_dev_ptr(t, group.numel, (dt,), f"dst[{i}]") for i, t in enumerate(dsts)])
+    _check(lib().tc_broadcast(group.handle, len(dsts), _dev_ptr(src, group.numel, (dt,), "src"), p, _DTYPES[dt],
+                              _stream(stream)))
+
+
+def broadcast_tensor(group: Group, K: int, src, dst, stream=None) -> None:
+    dt = _gdt(src)
+    _check(lib().tc_broadcast_tensor(group.handle, K, _dev_ptr(src, group.numel, (dt,), "src"),
+                                     _dev_ptr(dst, tensor_numel(group, K), (dt,), "dst"), _DTYPES[dt],
+                                     _stream(stream)))

@@ -342,3 +342,209 @@ TC_API int32_t easgd_step_tensor(const tc_group* g, int32_t K, float* x, const v
     if (e != hipSuccess) return hip_fail(e, "easgd_step_tensor launch");
     return TC_OK;
 }
+
+// ------------------------------------------- schedules and synchronous SGD
+
+namespace {
+
+// Shared checks of the separate-buffer step calls: K, finite scalars, the
+// device; returns TC_OK or an error (N == 0 is reported as TC_OK by the
+// caller before buffers are inspected).
+int32_t check_step(const tc_group* g, int32_t K, int32_t g_dtype, float s0, float s1) {
+    if (!g) return fail(TC_EINVAL, "group is NULL");
+    if (K < 1 || K > TC_MAX_K) { set_error("K = %d outside [1, %d]", K, TC_MAX_K); return TC_EINVAL; }
+    if (!elem_size(g_dtype)) { set_error("unknown dtype %d", g_dtype); return TC_EINVAL; }
+    if (!std::isfinite(s0) || !std::isfinite(s1)) return fail(TC_EINVAL, "step sizes must be finite");
+    return check_device(g);
+}
+
+// x[0..K) pairwise disjoint, each 4-byte aligned; *vec &= 16-byte aligned.
+int32_t check_workers(const tc_group* g, int32_t K, float* const* x, bool* vec) {
+    if (!x) return fail(TC_EINVAL, "NULL buffer array");
+    const int64_t xb = g->N * 4;
+    for (int32_t i = 0; i < K; ++i) {
+        if (!x[i]) { set_error("x[%d] is NULL", i); return TC_EINVAL; }
+        if (!aligned(x[i], 4)) { set_error("x[%d] misaligned", i); return TC_EINVAL; }
+        *vec = *vec && aligned(x[i], 16);
+        for (int32_t q = 0; q < i; ++q)
+            if (overlap(x[i], xb, x[q], xb)) { set_error("x[%d] overlaps x[%d]", i, q); return TC_EINVAL; }
+    }
+    return TC_OK;
+}
+
+// grad[0..K) element-aligned and disjoint from every x (and from each other
+// when `writable`).
+int32_t check_grads(const tc_group* g, int32_t K, const void* const* grad, int es, float* const* x, bool writable,
+                    bool* vec) {
+    if (!grad) return fail(TC_EINVAL, "NULL buffer array");
+    const int64_t gb = g->N * es, xb = g->N * 4;
+    for (int32_t i = 0; i < K; ++i) {
+        if (!grad[i]) { set_error("grad[%d] is NULL", i); return TC_EINVAL; }
+        if (!aligned(grad[i], es)) { set_error("grad[%d] misaligned", i); return TC_EINVAL; }
+        *vec = *vec && aligned(grad[i], es == 4 ? 16 : 8);
+        for (int32_t q = 0; q < K; ++q) {
+            if (overlap(grad[i], gb, x[q], xb)) { set_error("grad[%d] overlaps x[%d]", i, q); return TC_EINVAL; }
+            if (writable && q < i && overlap(grad[i], gb, grad[q], gb)) {
+                set_error("grad[%d] overlaps grad[%d]", i, q);
+                return TC_EINVAL;
+            }
+        }
+    }
+    return TC_OK;
+}
+
+int32_t launched(hipError_t e, const char* what) { return e == hipSuccess ? TC_OK : hip_fail(e, what); }
+
+int32_t check_tensor_step(const tc_group* g, const void* x, int64_t xbytes, const void* grad, int64_t gbytes) {
+    if (!x || (gbytes && !grad)) return fail(TC_EINVAL, "NULL buffer");
+    if (!aligned(x, 16) || (gbytes && !aligned(grad, 16)))
+        return fail(TC_EINVAL, "tensor-layout calls need 16-byte aligned buffers");
+    if (gbytes && overlap(x, xbytes, grad, gbytes)) return fail(TC_EINVAL, "x overlaps grad");
+    (void)g;
+    return TC_OK;
+}
+
+int32_t check_order(int32_t K, const int32_t* order, int32_t R) {
+    if (R < 0 || R > K) { set_error("R = %d outside [0, K = %d]", R, K); return TC_EINVAL; }
+    if (R && !order) return fail(TC_EINVAL, "order is NULL");
+    bool seen[TC_MAX_K] = {};
+    for (int32_t r = 0; r < R; ++r) {
+        if (order[r] < 0 || order[r] >= K) { set_error("order[%d] = %d outside [0, K)", r, order[r]); return TC_EINVAL; }
+        if (seen[order[r]]) { set_error("worker %d exchanges twice", order[r]); return TC_EINVAL; }
+        seen[order[r]] = true;
+    }
+    return TC_OK;
+}
+
+}  // namespace
+
+TC_API int32_t sgd_step(const tc_group* g, int32_t K, float* const* x, const void* const* grad, int32_t g_dtype,
+                        float eta, void* stream) {
+    clear_error();
+    if (int32_t r = check_step(g, K, g_dtype, eta, 0.0f)) return r;
+    if (g->N == 0) return TC_OK;
+    bool vec = true;
+    if (int32_t r = check_workers(g, K, x, &vec)) return r;
+    if (int32_t r = check_grads(g, K, grad, elem_size(g_dtype), x, false, &vec)) return r;
+    return launched(launch_sgd(K, x, grad, g_dtype, eta, g->N, vec, static_cast<hipStream_t>(stream)), "sgd_step launch");
+}
+
+TC_API int32_t sgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad, int32_t g_dtype, float eta,
+                               void* stream) {
+    clear_error();
+    if (int32_t r = check_step(g, K, g_dtype, eta, 0.0f)) return r;
+    if (g->N == 0) return TC_OK;
+    const int64_t tn = tc_tensor_numel(g, K);
+    if (int32_t r = check_tensor_step(g, x, tn * 4, grad, tn * elem_size(g_dtype))) return r;
+    return launched(launch_tensor_sgd(K, x, grad, g_dtype, eta, g->N, static_cast<hipStream_t>(stream)),
+                    "sgd_step_tensor launch");
+}
+
+TC_API int32_t easgd_period_step(const tc_group* g, int32_t K, float* const* x, const void* const* grad,
+                                 int32_t g_dtype, float* x_c, float eta, float rho, int64_t iteration, int32_t tau,
+                                 void* stream) {
+    clear_error();
+    if (tau < 1 || iteration < 0) { set_error("need tau >= 1 and iteration >= 0"); return TC_EINVAL; }
+    if (iteration % tau == 0) return easgd_step_ex(g, K, x, grad, g_dtype, x_c, eta, rho, stream);
+    return sgd_step(g, K, x, grad, g_dtype, eta, stream);
+}
+
+TC_API int32_t easgd_period_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad, int32_t g_dtype,
+                                        float* x_c, float eta, float rho, int64_t iteration, int32_t tau,
+                                        void* stream) {
+    clear_error();
+    if (tau < 1 || iteration < 0) { set_error("need tau >= 1 and iteration >= 0"); return TC_EINVAL; }
+    if (iteration % tau == 0) return easgd_step_tensor(g, K, x, grad, g_dtype, x_c, eta, rho, stream);
+    return sgd_step_tensor(g, K, x, grad, g_dtype, eta, stream);
+}
+
+TC_API int32_t elastic_async(const tc_group* g, int32_t K, float* const* x, float* x_c, const int32_t* order,
+                             int32_t R, float alpha, void* stream) {
+    clear_error();
+    if (int32_t r = check_step(g, K, TC_F32, alpha, 0.0f)) return r;
+    if (int32_t r = check_order(K, order, R)) return r;
+    if (g->N == 0 || R == 0) return TC_OK;
+    bool vec = true;
+    if (int32_t r = check_workers(g, K, x, &vec)) return r;
+    if (!x_c || !aligned(x_c, 4)) return fail(TC_EINVAL, "x_c is NULL or misaligned");
+    vec = vec && aligned(x_c, 16);
+    for (int32_t i = 0; i < K; ++i)
+        if (overlap(x[i], g->N * 4, x_c, g->N * 4)) { set_error("x[%d] overlaps x_c", i); return TC_EINVAL; }
+    return launched(launch_elastic_async(K, x, x_c, order, R, alpha, g->N, vec, static_cast<hipStream_t>(stream)),
+                    "elastic_async launch");
+}
+
+TC_API int32_t elastic_async_tensor(const tc_group* g, int32_t K, float* x, float* x_c, const int32_t* order,
+                                    int32_t R, float alpha, void* stream) {
+    clear_error();
+    if (int32_t r = check_step(g, K, TC_F32, alpha, 0.0f)) return r;
+    if (int32_t r = check_order(K, order, R)) return r;
+    if (g->N == 0 || R == 0) return TC_OK;
+    const int64_t tn = tc_tensor_numel(g, K);
+    if (int32_t r = check_tensor_step(g, x, tn * 4, x_c, g->N * 4)) return r;
+    return launched(launch_tensor_elastic_async(K, x, x_c, order, R, alpha, g->N, static_cast<hipStream_t>(stream)),
+                    "elastic_async_tensor launch");
+}
+
+TC_API int32_t sync_sgd_step(const tc_group* g, int32_t K, float* const* x, void* const* grad, int32_t g_dtype,
+                             float eta, float rescale, int32_t broadcast, void* stream) {
+    clear_error();
+    if (int32_t r = check_step(g, K, g_dtype, eta, rescale)) return r;
+    if (broadcast && g_dtype != TC_F32)
+        return fail(TC_EUNSUPPORTED, "broadcasting the summed gradient needs binary32 gradients");
+    if (g->N == 0) return TC_OK;
+    bool vec = true;
+    if (int32_t r = check_workers(g, K, x, &vec)) return r;
+    if (int32_t r = check_grads(g, K, const_cast<const void* const*>(grad), elem_size(g_dtype), x, broadcast != 0, &vec))
+        return r;
+    return launched(launch_sync_sgd(K, x, grad, g_dtype, eta, rescale, broadcast, g->N, vec,
+                                    static_cast<hipStream_t>(stream)),
+                    "sync_sgd_step launch");
+}
+
+TC_API int32_t sync_sgd_step_tensor(const tc_group* g, int32_t K, float* x, void* grad, int32_t g_dtype, float eta,
+                                    float rescale, int32_t broadcast, void* stream) {
+    clear_error();
+    if (int32_t r = check_step(g, K, g_dtype, eta, rescale)) return r;
+    if (broadcast && g_dtype != TC_F32)
+        return fail(TC_EUNSUPPORTED, "broadcasting the summed gradient needs binary32 gradients");
+    if (g->N == 0) return TC_OK;
+    const int64_t tn = tc_tensor_numel(g, K);
+    if (int32_t r = check_tensor_step(g, x, tn * 4, grad, tn * elem_size(g_dtype))) return r;
+    return launched(launch_tensor_sync_sgd(K, x, grad, g_dtype, eta, rescale, broadcast, g->N,
+                                           static_cast<hipStream_t>(stream)),
+                    "sync_sgd_step_tensor launch");
+}
+
+TC_API int32_t tc_broadcast(const tc_group* g, int32_t K, const void* src, void* const* dst, int32_t dtype,
+                            void* stream) {
+    clear_error();
+    if (int32_t r = check_step(g, K, dtype, 0.0f, 0.0f)) return r;
+    if (g->N == 0) return TC_OK;
+    const int es = elem_size(dtype);
+    const int64_t b = g->N * es;
+    if (!src || !dst) return fail(TC_EINVAL, "NULL buffer");
+    if (!aligned(src, es)) return fail(TC_EINVAL, "src misaligned");
+    bool vec = aligned(src, 16);
+    for (int32_t i = 0; i < K; ++i) {
+        if (!dst[i] || !aligned(dst[i], es)) { set_error("dst[%d] is NULL or misaligned", i); return TC_EINVAL; }
+        vec = vec && aligned(dst[i], 16);
+        if (overlap(dst[i], b, src, b)) { set_error("dst[%d] overlaps src", i); return TC_EINVAL; }
+        for (int32_t q = 0; q < i; ++q)
+            if (overlap(dst[i], b, dst[q], b)) { set_error("dst[%d] overlaps dst[%d]", i, q); return TC_EINVAL; }
+    }
+    return launched(launch_broadcast(K, src, dst, es, g->N, vec, static_cast<hipStream_t>(stream)), "tc_broadcast launch");
+}
+
+TC_API int32_t tc_broadcast_tensor(const tc_group* g, int32_t K, const void* src, void* dst, int32_t dtype,
+                                   void* stream) {
+    clear_error();
+    if (int32_t r = check_step(g, K, dtype, 0.0f, 0.0f)) return r;
+    if (g->N == 0) return TC_OK;
+    const int es = elem_size(dtype);
+    if (!src || !dst) return fail(TC_EINVAL, "NULL buffer");
+    if (!aligned(src, 16) || !aligned(dst, 16)) return fail(TC_EINVAL, "tensor-layout calls need 16-byte aligned buffers");
+    if (overlap(dst, tc_tensor_numel(g, K) * es, src, g->N * es)) return fail(TC_EINVAL, "dst overlaps src");
+    return launched(launch_tensor_broadcast(K, src, dst, es, g->N, static_cast<hipStream_t>(stream)),
+                    "tc_broadcast_tensor launch");
+}

@@ -284,14 +284,163 @@ __device__ __forceinline__ void easgd_any(const EasgdArgs<K, T>& a, I i, I du) {
     else easgd_slots<K, T, U, V, I>(a, i, du);
 }
 
+// ---------------------------------------------------- sgd / sync / async
+
+// Plain SGD on every worker: x_i = fma(-eta, g_i, x_i).
+template <int K, typename T>
+struct SgdArgs {
+    float* x[K];
+    const T* g[K];
+    float eta;
+    int k_total;
+};
+
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void sgd_slots(const SgdArgs<K, T>& a, I i, I du) {
+    if constexpr (K == TC_MAX_K) {
+        for (int q = 0; q < a.k_total; ++q) {  // workers one at a time
+            const V x = Mem<V>::load(a.x[q], i), g = Mem<V>::load(a.g[q], i);
+            Mem<V>::store(a.x[q], i, fmav(splat<V>(-a.eta), g, x));
+        }
+    } else {
+        V x[U][K], g[U][K];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int q = 0; q < K; ++q) {
+                x[u][q] = Mem<V>::load(a.x[q], i + I(u) * du);
+                g[u][q] = Mem<V>::load(a.g[q], i + I(u) * du);
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int q = 0; q < K; ++q) Mem<V>::store(a.x[q], i + I(u) * du, fmav(splat<V>(-a.eta), g[u][q], x[u][q]));
+    }
+}
+
+// Synchronous SGD through pushpull: S = pairwise sum of the K gradients,
+// x_i = fma(-eta*rescale, S, x_i) for every worker, and, when broadcast,
+// g_i = S (binary32 gradients only).
+template <int K, typename T>
+struct SyncArgs {
+    float* x[K];
+    T* g[K];
+    float step;  // eta * rescale, rounded once to binary32
+    int broadcast;
+    int k_total;
+};
+
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void sync_slots(const SyncArgs<K, T>& a, I i, I du) {
+    if constexpr (K == TC_MAX_K) {
+        constexpr int kParts = TC_MAX_K / kSpecialisedK;
+        V part[kParts];
+#pragma unroll
+        for (int c = 0; c < kParts; ++c) {
+            V v[kSpecialisedK];
+#pragma unroll
+            for (int q = 0; q < kSpecialisedK; ++q) {
+                const int k = c * kSpecialisedK + q;
+                v[q] = k < a.k_total ? Mem<V>::load(static_cast<const T*>(a.g[k]), i) : splat<V>(0.0f);
+            }
+            part[c] = Tree<kSpecialisedK>::sum(v);
+        }
+        const V S = Tree<kParts>::sum(part);
+        for (int q = 0; q < a.k_total; ++q) {
+            Mem<V>::store(a.x[q], i, fmav(splat<V>(-a.step), S, Mem<V>::load(a.x[q], i)));
+            if constexpr (sizeof(T) == 4)
+                if (a.broadcast) Mem<V>::store(a.g[q], i, S);
+        }
+    } else {
+        V g[U][K], x[U][K];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int q = 0; q < K; ++q) {
+                g[u][q] = Mem<V>::load(static_cast<const T*>(a.g[q]), i + I(u) * du);
+                x[u][q] = Mem<V>::load(a.x[q], i + I(u) * du);
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const V S = Tree<K>::sum(g[u]);
+#pragma unroll
+            for (int q = 0; q < K; ++q) {
+                Mem<V>::store(a.x[q], i + I(u) * du, fmav(splat<V>(-a.step), S, x[u][q]));
+                if constexpr (sizeof(T) == 4)
+                    if (a.broadcast) Mem<V>::store(a.g[q], i + I(u) * du, S);
+            }
+        }
+    }
+}
+
+// Asynchronous elastic exchanges: for r < R, worker w = order[r] (no worker
+// twice): d = x_w - c; c = fma(alpha, d, c); x_w = fma(-alpha, d, x_w).
+constexpr int kMaxOrder = TC_MAX_K;
+template <int K>
+struct AsyncArgs {
+    float* x[K];
+    float* xc;
+    uint8_t order[kMaxOrder];
+    int R;
+    float alpha;
+    int k_total;
+};
+
+template <int K, typename T>
+struct AsyncArgsT : AsyncArgs<K> {};
+
+template <int K, int U, typename V, typename I>
+__device__ __forceinline__ void async_slots(const AsyncArgs<K>& a, I i, I du) {
+    if constexpr (K == TC_MAX_K) {
+        V c = Mem<V>::load(a.xc, i);
+        for (int r = 0; r < a.R; ++r) {  // exchanges one at a time
+            float* xw = a.x[a.order[r]];
+            V x = Mem<V>::load(xw, i);
+            const V d = x - c;
+            c = fmav(splat<V>(a.alpha), d, c);
+            Mem<V>::store(xw, i, fmav(splat<V>(-a.alpha), d, x));
+        }
+        Mem<V>::store(a.xc, i, c);
+    } else {
+        // the (distinct) exchanged workers' values are all loaded first
+        V c[U], x[U][K];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            c[u] = Mem<V>::load(a.xc, i + I(u) * du);
+#pragma unroll
+            for (int r = 0; r < K; ++r)
+                if (r < a.R) x[u][r] = Mem<V>::load(a.x[a.order[r]], i + I(u) * du);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int r = 0; r < K; ++r)
+                if (r < a.R) {
+                    const V d = x[u][r] - c[u];
+                    c[u] = fmav(splat<V>(a.alpha), d, c[u]);
+                    x[u][r] = fmav(splat<V>(-a.alpha), d, x[u][r]);
+                }
+#pragma unroll
+            for (int r = 0; r < K; ++r)
+                if (r < a.R) Mem<V>::store(a.x[a.order[r]], i + I(u) * du, x[u][r]);
+            Mem<V>::store(a.xc, i + I(u) * du, c[u]);
+        }
+    }
+}
+
 // -------------------------------------------------------------- kernels
 
-// Op selects reduce or easgd through the argument type.
+// The operation is selected by the argument type.
 template <int K, typename T, int U, typename V, typename I>
 __device__ __forceinline__ void op_any(const ReduceArgs<K, T>& a, I i, I du) { reduce_any<K, T, U, V, I>(a, i, du); }
 template <int K, typename T, int U, typename V, typename I>
 __device__ __forceinline__ void op_any(const EasgdArgs<K, T>& a, I i, I du) { easgd_any<K, T, U, V, I>(a, i, du); }
-
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void op_any(const SgdArgs<K, T>& a, I i, I du) { sgd_slots<K, T, U, V, I>(a, i, du); }
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void op_any(const SyncArgs<K, T>& a, I i, I du) { sync_slots<K, T, U, V, I>(a, i, du); }
+template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void op_any(const AsyncArgsT<K, T>& a, I i, I du) { async_slots<K, U, V, I>(a, i, du); }
 // 16-byte slots, grid-stride; groups of U slots per lane, then the slots of
 // a last partial group one by one; the last workgroup does the < 4
 // trailing elements.
@@ -421,7 +570,151 @@ hipError_t dispatch_easgd(int K, float* const* x, const void* const* g, float* x
     }
 }
 
+// Broadcast of one flat buffer to K copies, bit for bit: 16-byte slots when
+// every buffer is 16-byte aligned, element by element otherwise; the last
+// workgroup copies the bytes after the last whole slot.
+struct BcastArgs {
+    const char* src;
+    char* dst[TC_MAX_K];
+    int K, es;
+    int64_t nbytes;
+};
+
+template <bool VEC>
+__global__ __launch_bounds__(TC_EW_THREADS) void bcast_kernel(BcastArgs a) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * TC_EW_THREADS;
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * TC_EW_THREADS + threadIdx.x;
+    if (VEC) {
+        const int64_t nvec = a.nbytes / 16;
+        for (int64_t v = t0; v < nvec; v += stride) {
+            const u4 w = __builtin_nontemporal_load(reinterpret_cast<const u4*>(a.src) + v);
+            for (int k = 0; k < a.K; ++k) __builtin_nontemporal_store(w, reinterpret_cast<u4*>(a.dst[k]) + v);
+        }
+        if (blockIdx.x == gridDim.x - 1)
+            for (int64_t b = nvec * 16 + threadIdx.x * a.es; b < a.nbytes; b += TC_EW_THREADS * a.es)
+                for (int k = 0; k < a.K; ++k) {
+                    if (a.es == 4) *reinterpret_cast<uint32_t*>(a.dst[k] + b) = *reinterpret_cast<const uint32_t*>(a.src + b);
+                    else *reinterpret_cast<uint16_t*>(a.dst[k] + b) = *reinterpret_cast<const uint16_t*>(a.src + b);
+                }
+    } else {
+        for (int64_t e = t0; e * a.es < a.nbytes; e += stride)
+            for (int k = 0; k < a.K; ++k) {
+                if (a.es == 4) reinterpret_cast<uint32_t*>(a.dst[k])[e] = reinterpret_cast<const uint32_t*>(a.src)[e];
+                else reinterpret_cast<uint16_t*>(a.dst[k])[e] = reinterpret_cast<const uint16_t*>(a.src)[e];
+            }
+    }
+}
+
+template <int K, typename T>
+hipError_t run_sgd(float* const* x, const void* const* g, float eta, int k_total, int64_t n, bool vec, hipStream_t s) {
+    SgdArgs<K, T> a{};
+    for (int q = 0; q < k_total; ++q) {
+        a.x[q] = x[q];
+        a.g[q] = static_cast<const T*>(g[q]);
+    }
+    a.eta = eta;
+    a.k_total = k_total;
+    return launch<K, T, easgd_unroll(K)>(a, n, vec, 4, s);
+}
+
+template <int K, typename T>
+hipError_t run_sync(float* const* x, void* const* g, float step, int broadcast, int k_total, int64_t n, bool vec,
+                    hipStream_t s) {
+    SyncArgs<K, T> a{};
+    for (int q = 0; q < k_total; ++q) {
+        a.x[q] = x[q];
+        a.g[q] = static_cast<T*>(g[q]);
+    }
+    a.step = step;
+    a.broadcast = broadcast;
+    a.k_total = k_total;
+    return launch<K, T, easgd_unroll(K)>(a, n, vec, 4, s);
+}
+
+template <int K, typename T>
+hipError_t run_async(float* const* x, float* xc, const int32_t* order, int R, float alpha, int k_total, int64_t n,
+                     bool vec, hipStream_t s) {
+    AsyncArgsT<K, T> a{};
+    for (int q = 0; q < k_total; ++q) a.x[q] = x[q];
+    for (int r = 0; r < R; ++r) a.order[r] = static_cast<uint8_t>(order[r]);
+    a.xc = xc;
+    a.R = R;
+    a.alpha = alpha;
+    a.k_total = k_total;
+    return launch<K, T, easgd_unroll(K)>(a, n, vec, 4, s);
+}
+
+template <typename T>
+hipError_t dispatch_sgd(int K, float* const* x, const void* const* g, float eta, int64_t n, bool vec, hipStream_t s) {
+    switch (K) {
+#define TC_CASE(k) \
+    case k: return run_sgd<k, T>(x, g, eta, K, n, vec, s);
+        TC_FOR_K(TC_CASE)
+#undef TC_CASE
+        default: return run_sgd<TC_MAX_K, T>(x, g, eta, K, n, vec, s);
+    }
+}
+
+template <typename T>
+hipError_t dispatch_sync(int K, float* const* x, void* const* g, float step, int broadcast, int64_t n, bool vec,
+                         hipStream_t s) {
+    switch (K) {
+#define TC_CASE(k) \
+    case k: return run_sync<k, T>(x, g, step, broadcast, K, n, vec, s);
+        TC_FOR_K(TC_CASE)
+#undef TC_CASE
+        default: return run_sync<TC_MAX_K, T>(x, g, step, broadcast, K, n, vec, s);
+    }
+}
+
+hipError_t dispatch_async(int K, float* const* x, float* xc, const int32_t* order, int R, float alpha, int64_t n,
+                          bool vec, hipStream_t s) {
+    switch (K) {
+#define TC_CASE(k) \
+    case k: return run_async<k, float>(x, xc, order, R, alpha, K, n, vec, s);
+        TC_FOR_K(TC_CASE)
+#undef TC_CASE
+        default: return run_async<TC_MAX_K, float>(x, xc, order, R, alpha, K, n, vec, s);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_sgd(int K, float* const* x, const void* const* g, int g_dtype, float eta, int64_t n, bool vector_ok,
+                      hipStream_t stream) {
+    if (g_dtype == TC_BF16) return dispatch_sgd<uint16_t>(K, x, g, eta, n, vector_ok, stream);
+    return dispatch_sgd<float>(K, x, g, eta, n, vector_ok, stream);
+}
+
+hipError_t launch_sync_sgd(int K, float* const* x, void* const* g, int g_dtype, float eta, float rescale, int broadcast,
+                           int64_t n, bool vector_ok, hipStream_t stream) {
+    const float step = eta * rescale;  // one binary32 rounding, on the host
+    if (g_dtype == TC_BF16) return dispatch_sync<uint16_t>(K, x, g, step, 0, n, vector_ok, stream);
+    return dispatch_sync<float>(K, x, g, step, broadcast, n, vector_ok, stream);
+}
+
+hipError_t launch_elastic_async(int K, float* const* x, float* xc, const int32_t* order, int R, float alpha,
+                                int64_t n, bool vector_ok, hipStream_t stream) {
+    return dispatch_async(K, x, xc, order, R, alpha, n, vector_ok, stream);
+}
+
+hipError_t launch_broadcast(int K, const void* src, void* const* dst, int es, int64_t n, bool vector_ok,
+                            hipStream_t stream) {
+    BcastArgs a{};
+    a.src = static_cast<const char*>(src);
+    for (int k = 0; k < K; ++k) a.dst[k] = static_cast<char*>(dst[k]);
+    a.K = K;
+    a.es = es;
+    a.nbytes = n * es;
+    if (vector_ok) {
+        dim3 grid(static_cast<unsigned>(grid_for(a.nbytes / 16, 1)));
+        hipLaunchKernelGGL((bcast_kernel<true>), grid, dim3(TC_EW_THREADS), 0, stream, a);
+    } else {
+        dim3 grid(static_cast<unsigned>(grid_for(n, 1)));
+        hipLaunchKernelGGL((bcast_kernel<false>), grid, dim3(TC_EW_THREADS), 0, stream, a);
+    }
+    return hipGetLastError();
+}
 
 hipError_t launch_reduce(int K, const void* const* in, int in_dtype, float* out, int op, int64_t n, bool vector_ok,
                          hipStream_t stream) {

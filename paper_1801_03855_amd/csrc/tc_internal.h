@@ -44,6 +44,15 @@ hipError_t launch_reduce(int K, const void* const* in, int in_dtype, float* out,
 hipError_t launch_easgd(int K, float* const* x, const void* const* g, int g_dtype, float* xc,
                         float eta, float rho, int64_t n, bool vector_ok, hipStream_t stream);
 
+hipError_t launch_sgd(int K, float* const* x, const void* const* g, int g_dtype, float eta, int64_t n, bool vector_ok,
+                      hipStream_t stream);
+hipError_t launch_sync_sgd(int K, float* const* x, void* const* g, int g_dtype, float eta, float rescale, int broadcast,
+                           int64_t n, bool vector_ok, hipStream_t stream);
+hipError_t launch_elastic_async(int K, float* const* x, float* xc, const int32_t* order, int R, float alpha,
+                                int64_t n, bool vector_ok, hipStream_t stream);
+hipError_t launch_broadcast(int K, const void* src, void* const* dst, int es, int64_t n, bool vector_ok,
+                            hipStream_t stream);
+
 hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, bool flat_aligned,
                        hipStream_t stream);
 
@@ -53,6 +62,12 @@ hipError_t launch_tensor_reduce(int K, const void* in, int in_dtype, float* out,
 hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, float* xc, float eta, float rho,
                                int64_t n, hipStream_t stream);
 hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStream_t stream);
+hipError_t launch_tensor_sgd(int K, float* x, const void* g, int g_dtype, float eta, int64_t n, hipStream_t s);
+hipError_t launch_tensor_sync_sgd(int K, float* x, void* g, int g_dtype, float eta, float rescale, int broadcast,
+                                  int64_t n, hipStream_t s);
+hipError_t launch_tensor_elastic_async(int K, float* x, float* xc, const int32_t* order, int R, float alpha, int64_t n,
+                                       hipStream_t s);
+hipError_t launch_tensor_broadcast(int K, const void* src, void* dst, int es, int64_t n, hipStream_t s);
 
 }  // namespace tc
 

@@ -263,6 +263,122 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
     }
 }
 
+// ------------------------------------------ sgd / sync / async / broadcast
+
+template <typename T>
+struct TStepArgs {
+    float* x;       // tensor layout, K copies
+    T* g;           // tensor layout, K copies (gradients)
+    float* xc;      // N values (async exchange)
+    int64_t nslot, n;
+    float s0, s1;   // sgd: eta; sync: eta*rescale; async: alpha
+    int K, flag;    // sync: broadcast the sum into g
+    uint8_t order[TC_MAX_K];
+    int R;
+};
+
+enum class TOp { Sgd, Sync, Async };
+
+__device__ __forceinline__ f4 shfl4(f4 v, int src) {
+    return f4{__shfl(v.x, src, 64), __shfl(v.y, src, 64), __shfl(v.z, src, 64), __shfl(v.w, src, 64)};
+}
+
+template <TOp OP, int P, typename T, typename I>
+__global__ __launch_bounds__(256) void tensor_step_kernel(TStepArgs<T> a) {
+    constexpr int SPW = 64 / P;
+    const int K = a.K;
+    const int i = threadIdx.x % P;
+    const I j = first_slot<P, 1, I>();
+    const I nslot = static_cast<I>(a.nslot);
+    const bool slot = j < nslot;
+    const bool live = slot && i < K;
+    const I piece = j * I(K) + I(i);
+    (void)SPW;
+    if constexpr (OP == TOp::Sgd) {
+        if (live) {
+            const f4 x = load_slot(a.x, piece), g = load_slot(static_cast<const T*>(a.g), piece);
+            store_slot(a.x, piece, fma4(f4(-a.s0), g, x));
+        }
+    } else if constexpr (OP == TOp::Sync) {
+        const f4 g = live ? load_slot(static_cast<const T*>(a.g), piece) : f4(0.0f);
+        const f4 x = live ? load_slot(a.x, piece) : f4(0.0f);
+        const f4 S = group_sum4<P>(g);
+        if (live) {
+            store_slot(a.x, piece, fma4(f4(-a.s0), S, x));
+            if constexpr (sizeof(T) == 4)
+                if (a.flag) store_slot(reinterpret_cast<float*>(a.g), piece, S);
+        }
+    } else {
+        // every lane of the slot's group runs the center's recurrence over
+        // the exchanges, taking the exchanged worker's values by shuffle
+        const f4 x = live ? load_slot(a.x, piece) : f4(0.0f);
+        f4 c = slot ? load_slot(a.xc, j) : f4(0.0f);
+        const int group = threadIdx.x & 63 & ~(P - 1);
+        f4 d_mine = f4(0.0f);
+        bool mine = false;
+        for (int r = 0; r < a.R; ++r) {
+            const int w = a.order[r];
+            const f4 xw = shfl4(x, group + w);
+            const f4 d = xw - c;
+            if (w == i) {
+                d_mine = d;
+                mine = true;
+            }
+            c = fma4(f4(a.s0), d, c);
+        }
+        if (live && mine) store_slot(a.x, piece, fma4(f4(-a.s0), d_mine, x));
+        if (slot && i == 0) store_slot(a.xc, j, c);
+    }
+    if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot, element by element
+        const int64_t e = 4 * a.nslot + threadIdx.x;
+        if (e < a.n) {
+            auto idx = [&](int q) { return (a.nslot * K + q) * 4 + (e & 3); };
+            if constexpr (OP == TOp::Sgd) {
+                for (int q = 0; q < K; ++q)
+                    a.x[idx(q)] = __builtin_fmaf(-a.s0, load_elem(static_cast<const T*>(a.g), idx(q)), a.x[idx(q)]);
+            } else if constexpr (OP == TOp::Sync) {
+                float t[P];
+#pragma unroll
+                for (int q = 0; q < P; ++q) t[q] = q < K ? load_elem(static_cast<const T*>(a.g), idx(q)) : 0.0f;
+                const float S = Tree<P>::sum(t);
+                for (int q = 0; q < K; ++q) {
+                    a.x[idx(q)] = __builtin_fmaf(-a.s0, S, a.x[idx(q)]);
+                    if constexpr (sizeof(T) == 4)
+                        if (a.flag) reinterpret_cast<float*>(a.g)[idx(q)] = S;
+                }
+            } else {
+                float c = a.xc[e];
+                for (int r = 0; r < a.R; ++r) {
+                    const int64_t k = idx(a.order[r]);
+                    const float d = a.x[k] - c;
+                    c = __builtin_fmaf(a.s0, d, c);
+                    a.x[k] = __builtin_fmaf(-a.s0, d, a.x[k]);
+                }
+                a.xc[e] = c;
+            }
+        }
+    }
+}
+
+// Broadcast of one flat buffer into every copy of a tensor-layout buffer.
+template <int P, typename T, typename I>
+__global__ __launch_bounds__(256) void tensor_bcast_kernel(const T* src, T* dst, int64_t nslot, int64_t n, int K) {
+    constexpr int SB = 4 * sizeof(T);
+    const int i = threadIdx.x % P;
+    const I j = first_slot<P, 1, I>();
+    if (j < static_cast<I>(nslot) && i < K) {
+        const char* sp = reinterpret_cast<const char*>(src) + j * I(SB);
+        char* dp = reinterpret_cast<char*>(dst) + (j * I(K) + I(i)) * I(SB);
+        if constexpr (SB == 16) __builtin_nontemporal_store(*reinterpret_cast<const u4*>(sp), reinterpret_cast<u4*>(dp));
+        else __builtin_nontemporal_store(*reinterpret_cast<const u2*>(sp), reinterpret_cast<u2*>(dp));
+    }
+    if (blockIdx.x == gridDim.x - 1) {
+        const int64_t e = 4 * nslot + threadIdx.x;
+        if (e < n)
+            for (int q = 0; q < K; ++q) dst[(nslot * K + q) * 4 + (e & 3)] = src[e];
+    }
+}
+
 // ------------------------------------------------------- pack / unpack
 
 struct TPackArgs {
@@ -611,6 +727,86 @@ hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack
     switch (next_pow2(tl->K)) {
 #define TC_CASE(p) \
     case p: return run_tpack<p>(a, tl->elem, unpack, blocks, stream);
+        TC_FOR_P(TC_CASE)
+#undef TC_CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <TOp OP, int P, typename T>
+hipError_t run_tstep(const TStepArgs<T>& a, hipStream_t s) {
+    constexpr int SPB = 256 / P;
+    const int64_t blocks = (a.nslot + SPB - 1) / SPB;
+    dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+    if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
+        hipLaunchKernelGGL((tensor_step_kernel<OP, P, T, uint32_t>), grid, dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((tensor_step_kernel<OP, P, T, int64_t>), grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+template <TOp OP, typename T>
+hipError_t dispatch_tstep(const TStepArgs<T>& a, hipStream_t s) {
+    switch (next_pow2(a.K)) {
+#define TC_CASE(p) \
+    case p: return run_tstep<OP, p, T>(a, s);
+        TC_FOR_P(TC_CASE)
+#undef TC_CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <TOp OP>
+hipError_t tstep(int K, float* x, void* g, int g_dtype, float* xc, float s0, int flag, const int32_t* order, int R,
+                 int64_t n, hipStream_t s) {
+    if (g_dtype == TC_BF16) {
+        TStepArgs<uint16_t> a{};
+        a.x = x; a.g = static_cast<uint16_t*>(g); a.xc = xc; a.nslot = n / 4; a.n = n; a.s0 = s0; a.K = K; a.flag = flag;
+        for (int r = 0; r < R; ++r) a.order[r] = static_cast<uint8_t>(order[r]);
+        a.R = R;
+        return dispatch_tstep<OP, uint16_t>(a, s);
+    }
+    TStepArgs<float> a{};
+    a.x = x; a.g = static_cast<float*>(g); a.xc = xc; a.nslot = n / 4; a.n = n; a.s0 = s0; a.K = K; a.flag = flag;
+    for (int r = 0; r < R; ++r) a.order[r] = static_cast<uint8_t>(order[r]);
+    a.R = R;
+    return dispatch_tstep<OP, float>(a, s);
+}
+
+hipError_t launch_tensor_sgd(int K, float* x, const void* g, int g_dtype, float eta, int64_t n, hipStream_t s) {
+    return tstep<TOp::Sgd>(K, x, const_cast<void*>(g), g_dtype, nullptr, eta, 0, nullptr, 0, n, s);
+}
+
+hipError_t launch_tensor_sync_sgd(int K, float* x, void* g, int g_dtype, float eta, float rescale, int broadcast,
+                                  int64_t n, hipStream_t s) {
+    const float step = eta * rescale;  // one binary32 rounding, on the host
+    return tstep<TOp::Sync>(K, x, g, g_dtype, nullptr, step, g_dtype == TC_BF16 ? 0 : broadcast, nullptr, 0, n, s);
+}
+
+hipError_t launch_tensor_elastic_async(int K, float* x, float* xc, const int32_t* order, int R, float alpha, int64_t n,
+                                       hipStream_t s) {
+    return tstep<TOp::Async>(K, x, nullptr, TC_F32, xc, alpha, 0, order, R, n, s);
+}
+
+template <int P, typename T>
+hipError_t run_tbcast(const void* src, void* dst, int K, int64_t n, hipStream_t s) {
+    constexpr int SPB = 256 / P;
+    const int64_t nslot = n / 4;
+    const int64_t blocks = (nslot + SPB - 1) / SPB;
+    dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+    if ((nslot + 1) * K * 16 < (int64_t(1) << 32))
+        hipLaunchKernelGGL((tensor_bcast_kernel<P, T, uint32_t>), grid, dim3(256), 0, s, static_cast<const T*>(src),
+                           static_cast<T*>(dst), nslot, n, K);
+    else
+        hipLaunchKernelGGL((tensor_bcast_kernel<P, T, int64_t>), grid, dim3(256), 0, s, static_cast<const T*>(src),
+                           static_cast<T*>(dst), nslot, n, K);
+    return hipGetLastError();
+}
+
+hipError_t launch_tensor_broadcast(int K, const void* src, void* dst, int es, int64_t n, hipStream_t s) {
+    switch (next_pow2(K)) {
+#define TC_CASE(p) \
+    case p: return es == 2 ? run_tbcast<p, uint16_t>(src, dst, K, n, s) : run_tbcast<p, uint32_t>(src, dst, K, n, s);
         TC_FOR_P(TC_CASE)
 #undef TC_CASE
         default: return hipErrorInvalidValue;
