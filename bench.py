@@ -219,6 +219,66 @@ def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
     return {"step_ms": step_ms, "per_op_ms": per_op_ms}
 
 
+def next_rows(tc, wl, steps=20):
+    """Per-op bandwidth of the schedule and synchronous-SGD operations on the
+    ResNet-50 group, K = 8, binary32, both layouts (HIP events on the
+    stream; algorithmic bytes as in op_bytes)."""
+    import torch
+
+    w = wl.WORKLOADS["resnet50_k8_easgd"]
+    sizes = w.sizes()
+    g = tc.Group(sizes)
+    N, K, dev = g.numel, w.K, "cuda"
+    stream = torch.cuda.current_stream()
+    order = list(range(K))
+    xs, xc = wl.make_state(w, N, dev)
+    gs = wl.make_gradients(w, N, dev)
+    src = torch.randn(N, device=dev)
+    dsts = [torch.empty(N, device=dev) for _ in range(K)]
+    X = torch.empty(tc.tensor_numel(g, K), device=dev)
+    G = torch.empty(tc.tensor_numel(g, K), device=dev)
+    tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X, stream)
+    tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in gs]), G, stream)
+    bytes_ = {"sgd": 12 * K * N, "elastic_async": (8 * K + 8) * N, "sync_sgd_broadcast": 16 * K * N,
+              "broadcast": (4 + 4 * K) * N}
+    ops = {
+        "separate": {
+            "sgd": lambda: tc.sgd_step(g, xs, gs, 1e-6, stream),
+            "elastic_async": lambda: tc.elastic_async(g, xs, xc, order, 0.1125, stream),
+            "sync_sgd_broadcast": lambda: tc.sync_sgd_step(g, xs, gs, 1e-6, 1.0, True, stream),
+            "broadcast": lambda: tc.broadcast(g, src, dsts, stream),
+        },
+        "tensor": {
+            "sgd": lambda: tc.sgd_step_tensor(g, K, X, G, 1e-6, stream),
+            "elastic_async": lambda: tc.elastic_async_tensor(g, K, X, xc, order, 0.1125, stream),
+            "sync_sgd_broadcast": lambda: tc.sync_sgd_step_tensor(g, K, X, G, 1e-6, 1.0, True, stream),
+            "broadcast": lambda: tc.broadcast_tensor(g, K, src, X, stream),
+        },
+    }
+    out = {}
+    for lay, table in ops.items():
+        out[lay] = {}
+        for name, fn in table.items():
+            for _ in range(3):
+                fn()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record(stream)
+            for _ in range(steps):
+                fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(b) / steps
+            gbs = bytes_[name] / (ms * 1e-3) / 1e9
+            out[lay][name] = {"ms": round(ms, 5), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    # the periodic schedule (tau = 64): 63 SGD steps and one elastic step
+    for lay in out:
+        out[lay]["easgd_period_tau64_bytes_per_iter"] = round((63 * bytes_["sgd"] + 104 * N) / 64)
+    del xs, gs, X, G, dsts
+    torch.cuda.empty_cache()
+    return {"workload": "ResNet-50 group, K=8, binary32", "ops": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -230,6 +290,8 @@ def main():
                          "(default: the workload's faster one)")
     ap.add_argument("--no-compare", action="store_true", help="skip the other layout")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-next-rows", action="store_true",
+                    help="skip timing the schedule and synchronous-SGD operations")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="only run one plain device copy of 1 GiB (read 1 GiB, write 1 GiB), the known "
                          "reference for scaling hardware byte counters, and exit")
@@ -292,6 +354,11 @@ def main():
         layouts[lay] = {"value": round(step_bytes / (r["step_ms"] * 1e-3) / 1e9, 2), "ms_per_step": round(r["step_ms"], 5),
                         "kernels": kernel_table(r["per_op_ms"])}
 
+    extra = None
+    if not args.no_next_rows and args.workload == "resnet50_k8_pipeline":
+        print("# schedule and synchronous-SGD operations", file=sys.stderr, flush=True)
+        extra = next_rows(tc, wl)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle, 1 thread)", file=sys.stderr, flush=True)
@@ -316,6 +383,7 @@ def main():
         "kernels": kernels,
         "layouts": layouts,
         "roofline": roof,
+        "next_rows": extra,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
