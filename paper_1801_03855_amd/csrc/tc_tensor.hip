@@ -279,10 +279,6 @@ struct TStepArgs {
 
 enum class TOp { Sgd, Sync, Async };
 
-__device__ __forceinline__ f4 shfl4(f4 v, int src) {
-    return f4{__shfl(v.x, src, 64), __shfl(v.y, src, 64), __shfl(v.z, src, 64), __shfl(v.w, src, 64)};
-}
-
 template <TOp OP, int P, typename T, typename I>
 __global__ __launch_bounds__(256) void tensor_step_kernel(TStepArgs<T> a) {
     constexpr int SPW = 64 / P;
@@ -310,16 +306,19 @@ __global__ __launch_bounds__(256) void tensor_step_kernel(TStepArgs<T> a) {
         }
     } else {
         // every lane of the slot's group runs the center's recurrence over
-        // the exchanges, taking the exchanged worker's values by shuffle
+        // the exchanges, reading the exchanged worker's slot from LDS (one
+        // broadcast read per exchange)
+        __shared__ f4 s_x[256];
         const f4 x = live ? load_slot(a.x, piece) : f4(0.0f);
         f4 c = slot ? load_slot(a.xc, j) : f4(0.0f);
-        const int group = threadIdx.x & 63 & ~(P - 1);
+        s_x[threadIdx.x] = x;
+        __syncthreads();
+        const int group = threadIdx.x & ~(P - 1);
         f4 d_mine = f4(0.0f);
         bool mine = false;
         for (int r = 0; r < a.R; ++r) {
             const int w = a.order[r];
-            const f4 xw = shfl4(x, group + w);
-            const f4 d = xw - c;
+            const f4 d = s_x[group + w] - c;
             if (w == i) {
                 d_mine = d;
                 mine = true;
