@@ -14,7 +14,10 @@ The K copies are held either in the tensor layout (one buffer, copies
 interleaved in slots of four elements: tc_pack_tensor, tc_reduce_tensor,
 easgd_step_tensor, tc_unpack_tensor), the headline, or as K separate flat
 buffers (tc_pack, tc_reduce, easgd_step, tc_unpack), measured in the same
-run and reported beside it.  The bytes moved are the same.
+run and reported beside it.  The bytes moved are the same.  The same run
+also times the whole step as one launch (easgd_pipeline_tensor: the four
+operations with the intermediates kept on chip, 172 instead of 268 bytes
+per element at K = 8) and reports it under fused_pipeline.
 
 Inputs are seeded synthetic values resident in HBM before timing starts.
 The reported value is the step's algorithmic HBM traffic (every input read
@@ -219,6 +222,50 @@ def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
     return {"step_ms": step_ms, "per_op_ms": per_op_ms}
 
 
+def fused_bytes(K: int, N: int, s_g: int, write_g: bool = True) -> int:
+    """Algorithmic bytes of the one-pass pipeline: read the K gradient
+    lists, the K workers and the center; write the packed gradients (when
+    asked), the AVG, the K workers, the center and the K parameter lists."""
+    return ((2 * s_g if write_g else s_g) + 12) * K * N + 12 * N
+
+
+def run_fused(tc, wl, w, sizes, g, steps, warmup):
+    """The whole step as one easgd_pipeline_tensor launch, with and without
+    writing the packed gradients; average step times (ms) from HIP events on
+    the stream."""
+    import torch
+
+    N, K = g.numel, w.K
+    dev = "cuda"
+    gdt = torch.bfloat16 if w.g_dtype == "bf16" else torch.float32
+    print(f"# setup one-pass pipeline: n={len(sizes)} N={N} K={K}", file=sys.stderr, flush=True)
+    grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in wl.make_gradients(w, N, dev)])
+    xs, xc = wl.make_state(w, N, dev)
+    X = torch.empty(tc.tensor_numel(g, K), dtype=torch.float32, device=dev)
+    tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
+    del xs
+    G = torch.empty(tc.tensor_numel(g, K), dtype=gdt, device=dev)
+    gbar = torch.empty(N, dtype=torch.float32, device=dev)
+    params = tc.TensorList(g, [[torch.empty(s, dtype=torch.float32, device=dev) for s in sizes] for _ in range(K)])
+    stream = torch.cuda.current_stream()
+    out = {}
+    for write_g in (True, False):
+        gt = G if write_g else None
+        for _ in range(warmup):
+            tc.easgd_pipeline_tensor(grads, params, gt, gbar, X, xc, w.eta, w.rho, stream)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(steps):
+            tc.easgd_pipeline_tensor(grads, params, gt, gbar, X, xc, w.eta, w.rho, stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        out[write_g] = a.elapsed_time(b) / steps
+    del grads, X, G, gbar, params, xc
+    torch.cuda.empty_cache()
+    return out
+
+
 def next_rows(tc, wl, steps=20):
     """Per-op bandwidth of the schedule and synchronous-SGD operations on the
     ResNet-50 group, K = 8, binary32, both layouts (HIP events on the
@@ -290,6 +337,8 @@ def main():
                          "(default: the workload's faster one)")
     ap.add_argument("--no-compare", action="store_true", help="skip the other layout")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fused", action="store_true",
+                    help="skip timing the one-pass pipeline (easgd_pipeline_tensor)")
     ap.add_argument("--no-next-rows", action="store_true",
                     help="skip timing the schedule and synchronous-SGD operations")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -354,6 +403,18 @@ def main():
         layouts[lay] = {"value": round(step_bytes / (r["step_ms"] * 1e-3) / 1e9, 2), "ms_per_step": round(r["step_ms"], 5),
                         "kernels": kernel_table(r["per_op_ms"])}
 
+    fused = None
+    if not args.no_fused and set(ops) == {"pack", "reduce", "easgd", "unpack"}:
+        ft = run_fused(tc, wl, w, sizes, g, args.steps, args.warmup)
+        four_ms = results["tensor"]["step_ms"] if "tensor" in results else None
+        fused = {"entry_point": "easgd_pipeline_tensor", "layout": "tensor"}
+        for write_g, key in ((True, "with_packed_gradients"), (False, "without_packed_gradients")):
+            b = fused_bytes(K, N, s_g, write_g)
+            gbs = b / (ft[write_g] * 1e-3) / 1e9
+            fused[key] = {"ms_per_step": round(ft[write_g], 5), "steps_per_s": round(1e3 / ft[write_g], 2),
+                          "algorithmic_bytes": b, "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+                          "speedup_vs_four_calls": round(four_ms / ft[write_g], 3) if four_ms else None}
+
     extra = None
     if not args.no_next_rows and args.workload == "resnet50_k8_pipeline":
         print("# schedule and synchronous-SGD operations", file=sys.stderr, flush=True)
@@ -383,6 +444,7 @@ def main():
         "kernels": kernels,
         "layouts": layouts,
         "roofline": roof,
+        "fused_pipeline": fused,
         "next_rows": extra,
         "cpu_baseline": cpu,
     }

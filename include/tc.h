@@ -285,7 +285,7 @@ int32_t elastic_async_tensor(const tc_group* g, int32_t K, float* x, float* x_c,
 
 /* ------------------------------------------------------------------------
  * sync_sgd_step: synchronous SGD through pushpull (Sec. 5, the synchronous
- * SGD listing; Sec. 3.2, pushpull): with S = the pairwise sum of the K
+ * SGD listing; Sec. 4.2, pushpull): with S = the pairwise sum of the K
  * gradients (the value push and pull leave in every worker's gradient),
  *     x[i][j] = fma(-(eta*rescale), S[j], x[i][j])   for every worker i,
  * eta*rescale rounded once to binary32 (rescale = 1/mini_batch_size
@@ -315,6 +315,34 @@ int32_t tc_broadcast(const tc_group* g, int32_t K, const void* src, void* const*
  * aligned src and dst). */
 int32_t tc_broadcast_tensor(const tc_group* g, int32_t K, const void* src, void* dst,
                             int32_t dtype, void* stream);
+
+/* ------------------------------------------------------------------------
+ * easgd_pipeline_tensor: the whole step in one pass over the tensor layout.
+ * Equivalent, bit for bit, to the four calls
+ *     tc_pack_tensor(grads, g_tensor);
+ *     tc_reduce_tensor(g, K, g_tensor, grads' dtype, gbar, TC_AVG);
+ *     easgd_step_tensor(g, K, x, g_tensor, grads' dtype, x_c, eta, rho);
+ *     tc_unpack_tensor(params, x);
+ * but each workgroup takes its chunk of the group through all four with the
+ * intermediates on chip, so the gradients are read once and the new workers
+ * are not read back: the on-chip form of pipelining the pieces of a chunked
+ * reduction through its stages (Sec. 6.3.2, the multi-ring listing), for
+ * the push (Sec. 3.2: gather and sum a key's tensors), the elastic update
+ * (Sec. 2.2, Eqs. 2 and 3, summed over K workers, with the SGD move of
+ * Sec. 2.1) and the pull (Sec. 3.2: copy to every tensor of the list).
+ *
+ * grads: K*n gradient tensors (TC_F32 or TC_BF16); params: K*n binary32
+ * tensors; both lists of the same group object and K.  g_tensor: the packed
+ * gradients in the tensor layout (tc_tensor_numel(g, K) elements of the
+ * gradient dtype), or NULL to leave them unwritten.  gbar: N binary32
+ * values (the AVG).  x: the K binary32 workers in the tensor layout (in/out).
+ * x_c: N binary32 values (in/out).  Every flat buffer 16-byte aligned and
+ * disjoint from the others; the per-layer tensors must not overlap any flat
+ * buffer or each other (not checked).  eta, rho finite.  TC_EINVAL on bad
+ * arguments.
+ * ---------------------------------------------------------------------- */
+int32_t easgd_pipeline_tensor(const tc_tensorlist* grads, const tc_tensorlist* params, void* g_tensor,
+                              float* gbar, float* x, float* x_c, float eta, float rho, void* stream);
 
 #ifdef __cplusplus
 }

@@ -33,7 +33,7 @@
  *                   (Elastic1) and the worker moves toward the center
  *                   (Elastic2), workers in arrival order.
  *   sync pushpull   Sec. 5, synchronous SGD: push and pull (or pushpull,
- *                   Sec. 3.2) leave every worker's gradient equal to the sum
+ *                   Sec. 4.2) leave every worker's gradient equal to the sum
  *                   over the workers; SGD.Update then applies it with rescale
  *                   1/mini_batch_size.
  *   broadcast       Sec. 3.2: pull copies one value to every tensor of the

@@ -100,6 +100,7 @@ def lib(path: str = LIBRARY) -> ctypes.CDLL:
         "sync_sgd_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, f32, f32, i32, _VP]),
         "tc_broadcast": (i32, [_VP, i32, _VP, _VPP, i32, _VP]),
         "tc_broadcast_tensor": (i32, [_VP, i32, _VP, _VP, i32, _VP]),
+        "easgd_pipeline_tensor": (i32, [_VP, _VP, _VP, _VP, _VP, _VP, f32, f32, _VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -393,3 +394,24 @@ def broadcast_tensor(group: Group, K: int, src, dst, stream=None) -> None:
     _check(lib().tc_broadcast_tensor(group.handle, K, _dev_ptr(src, group.numel, (dt,), "src"),
                                      _dev_ptr(dst, tensor_numel(group, K), (dt,), "dst"), _DTYPES[dt],
                                      _stream(stream)))
+
+
+# ----------------------------------------------------------------- pipeline
+
+def easgd_pipeline_tensor(grads: TensorList, params: TensorList, g_tensor: Optional[torch.Tensor],
+                          gbar: torch.Tensor, x: torch.Tensor, xc: torch.Tensor, eta: float, rho: float,
+                          stream=None) -> None:
+    """The whole step in one pass (easgd_pipeline_tensor): pack the gradient
+    lists into g_tensor (skipped when None), gbar = their AVG, the fused
+    elastic step on the tensor-layout workers x and the center xc, and the
+    new workers unpacked into the parameter lists."""
+    if grads.group is not params.group:
+        raise ValueError("the gradient and parameter lists must share one group")
+    group, K = grads.group, grads.K
+    n = tensor_numel(group, K)
+    gt = _dev_ptr(g_tensor, n, (grads.dtype,), "g_tensor") if g_tensor is not None else None
+    _check(lib().easgd_pipeline_tensor(grads.handle, params.handle, gt,
+                                       _dev_ptr(gbar, group.numel, (torch.float32,), "gbar"),
+                                       _dev_ptr(x, n, (torch.float32,), "x"),
+                                       _dev_ptr(xc, group.numel, (torch.float32,), "x_c"), float(eta), float(rho),
+                                       _stream(stream)))

@@ -548,3 +548,32 @@ TC_API int32_t tc_broadcast_tensor(const tc_group* g, int32_t K, const void* src
     return launched(launch_tensor_broadcast(K, src, dst, es, g->N, static_cast<hipStream_t>(stream)),
                     "tc_broadcast_tensor launch");
 }
+
+// ------------------------------------------------------------ pipeline
+
+TC_API int32_t easgd_pipeline_tensor(const tc_tensorlist* grads, const tc_tensorlist* params, void* g_tensor,
+                                     float* gbar, float* x, float* x_c, float eta, float rho, void* stream) {
+    clear_error();
+    if (!grads || !params) return fail(TC_EINVAL, "NULL tensor list");
+    const tc_group* g = grads->g;
+    if (params->g != g) return fail(TC_EINVAL, "the gradient and parameter lists belong to different groups");
+    if (params->K != grads->K) return fail(TC_EINVAL, "the gradient and parameter lists have different K");
+    if (params->dtype != TC_F32) return fail(TC_EINVAL, "parameter tensors must be binary32");
+    if (!std::isfinite(eta) || !std::isfinite(rho)) return fail(TC_EINVAL, "eta and rho must be finite");
+    if (int32_t r = check_device(g)) return r;
+    if (g->N == 0) return TC_OK;
+    if (!gbar || !x || !x_c) return fail(TC_EINVAL, "NULL buffer");
+    if (!aligned(gbar, 16) || !aligned(x, 16) || !aligned(x_c, 16) || (g_tensor && !aligned(g_tensor, 16)))
+        return fail(TC_EINVAL, "tensor-layout calls need 16-byte aligned buffers");
+    const int K = grads->K;
+    const int64_t tn = tc_tensor_numel(g, K), nb = g->N * 4;
+    const int64_t gtb = g_tensor ? tn * grads->elem : 0;
+    if (overlap(x, tn * 4, x_c, nb)) return fail(TC_EINVAL, "x overlaps x_c");
+    if (overlap(x, tn * 4, gbar, nb)) return fail(TC_EINVAL, "x overlaps gbar");
+    if (overlap(x_c, nb, gbar, nb)) return fail(TC_EINVAL, "x_c overlaps gbar");
+    if (gtb && (overlap(g_tensor, gtb, x, tn * 4) || overlap(g_tensor, gtb, x_c, nb) || overlap(g_tensor, gtb, gbar, nb)))
+        return fail(TC_EINVAL, "g_tensor overlaps another buffer");
+    return launched(launch_tensor_pipeline(grads, params, g_tensor, gbar, x, x_c, eta, rho,
+                                           static_cast<hipStream_t>(stream)),
+                    "easgd_pipeline_tensor launch");
+}

@@ -68,6 +68,8 @@ hipError_t launch_tensor_sync_sgd(int K, float* x, void* g, int g_dtype, float e
 hipError_t launch_tensor_elastic_async(int K, float* x, float* xc, const int32_t* order, int R, float alpha, int64_t n,
                                        hipStream_t s);
 hipError_t launch_tensor_broadcast(int K, const void* src, void* dst, int es, int64_t n, hipStream_t s);
+hipError_t launch_tensor_pipeline(const tc_tensorlist* grads, const tc_tensorlist* params, void* gt, float* gbar,
+                                  float* x, float* xc, float eta, float rho, hipStream_t stream);
 
 }  // namespace tc
 

@@ -629,6 +629,268 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
     }
 }
 
+// ------------------------------------------------------------ pipeline
+
+// The whole step in one pass: pack the K gradient lists into the tensor
+// layout, average them, take the fused elastic step, and unpack the K new
+// workers into their per-layer tensors.  The same arithmetic as tc_pack_tensor,
+// tc_reduce_tensor (AVG), easgd_step_tensor and tc_unpack_tensor in turn, but
+// each workgroup takes its chunk of the group through all four with the
+// intermediates in LDS and registers: the gradients are read from HBM once
+// (not three times) and the new workers are not read back for the unpack.
+// This is the on-chip form of pipelining a chunked reduction (Sec. 6.3.2: a
+// message split so that its pieces flow through the stages concurrently);
+// on one GPU, pipelining across kernel launches loses ~8 us per launch to
+// drain and ramp-up and gains nothing from the last-level cache.
+//
+// Per tile of M slots:
+//   gather   lanes walk consecutive slots of one copy's gradient tensors
+//            (as tc_pack_tensor) into the LDS tile; the workers and the
+//            center of the same slots are loaded in tensor order meanwhile;
+//   step     lanes take pieces in tensor order (P lanes per slot, lane i =
+//            worker i, as easgd_step_tensor): the packed gradients are
+//            written out (optional), the AVG and the center's spread are
+//            split butterflies (as tc_reduce_tensor), the workers' new
+//            values go to HBM and to the tile;
+//   scatter  lanes walk consecutive slots of one copy's parameter tensors
+//            (as tc_unpack_tensor); tile edges count as ends of a run of
+//            whole slots, so a misaligned destination never needs a slot of
+//            the next tile.
+struct TPipeArgs {
+    const int64_t* offsets;
+    const int32_t* chunk_first;
+    void* const* gptrs;  // K*n gradient tensors, copy-major
+    void* const* xptrs;  // K*n binary32 parameter tensors, copy-major
+    void* gt;            // packed gradients, tensor layout, or null
+    float* gbar;         // N values: the AVG of the K gradients
+    float* x;            // workers, tensor layout
+    float* xc;           // N values: the center
+    int32_t n, K;
+    int64_t N, chunk;
+    float eta, rho, a;
+};
+
+constexpr int kPipeStage = 512;
+
+__device__ __forceinline__ f4 widen_piece(u4 v, int es) {
+    if (es == 4) return f4{__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w)};
+    return f4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
+              __uint_as_float(v.y & 0xffff0000u)};
+}
+
+__device__ __forceinline__ float comp(f4 v, int c) { return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w; }
+
+template <int P, typename T, bool WG>
+__global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
+    constexpr int ES = sizeof(T);
+    constexpr int SB = 4 * ES;                         // gradient slot bytes
+    constexpr int M = 1024 / P > 16 ? 1024 / P : 16;   // slots per tile
+    constexpr int R = (M * P) / 256;                   // pieces per lane and phase
+    constexpr int ROWG = (P + 1) * SB, ROWX = (P + 1) * 16;
+    __shared__ int32_t s_rel[kPipeStage + 1];
+    __shared__ uintptr_t s_gbase[kPipeStage];
+    __shared__ uintptr_t s_xbase[kPipeStage];
+    __shared__ __attribute__((aligned(16))) unsigned char s_tile[M * ROWX];
+    const int K = a.K;
+    const int i = threadIdx.x % P;
+    const int64_t cstart = static_cast<int64_t>(blockIdx.x) * a.chunk;
+    const int32_t clen = static_cast<int32_t>(a.N - cstart < a.chunk ? a.N - cstart : a.chunk);
+    const int32_t lo = a.chunk_first[blockIdx.x];
+    const int32_t hi = a.chunk_first[blockIdx.x + 1];
+    const int nseg = hi - lo + 1;
+    const bool rel_staged = nseg <= kPipeStage;
+    const bool base_staged = static_cast<int64_t>(nseg) * K <= kPipeStage;
+    auto rel_global = [&](int s) -> int32_t { return clamp_rel(a.offsets[lo + s] - cstart, clen); };
+    auto base_global = [&](void* const* ptrs, int es, int kk, int s) -> uintptr_t {
+        return reinterpret_cast<uintptr_t>(ptrs[static_cast<int64_t>(kk) * a.n + lo + s]) -
+               static_cast<uintptr_t>((a.offsets[lo + s] - cstart) * es);
+    };
+    if (rel_staged)
+        for (int s = threadIdx.x; s <= nseg; s += 256) s_rel[s] = rel_global(s);
+    if (base_staged)
+        for (int q = threadIdx.x; q < nseg * K; q += 256) {
+            s_gbase[q] = base_global(a.gptrs, ES, q / nseg, q % nseg);
+            s_xbase[q] = base_global(a.xptrs, 4, q / nseg, q % nseg);
+        }
+    __syncthreads();
+    auto rel = [&](int s) -> int32_t { return rel_staged ? s_rel[s] : rel_global(s); };
+    auto gbase = [&](int kk, int s) -> uintptr_t {
+        return base_staged ? s_gbase[kk * nseg + s] : base_global(a.gptrs, ES, kk, s);
+    };
+    auto xbase = [&](int kk, int s) -> uintptr_t {
+        return base_staged ? s_xbase[kk * nseg + s] : base_global(a.xptrs, 4, kk, s);
+    };
+    auto find = [&](int jr) {  // last segment whose start is <= jr
+        int l = 0, h = nseg - 1;
+        while (l < h) {
+            const int mid = (l + h + 1) >> 1;
+            if (rel(mid) <= jr) l = mid; else h = mid - 1;
+        }
+        return l;
+    };
+    auto gtile = [&](int jl, int kk) -> unsigned char* { return s_tile + jl * ROWG + kk * SB; };
+    auto xtile = [&](int jl, int kk) -> unsigned char* { return s_tile + jl * ROWX + kk * 16; };
+    const int64_t slot0 = cstart / 4;
+    const f4 rho = f4(a.rho), neg_eta = f4(-a.eta), alpha = f4(a.a);
+    const float kf = static_cast<float>(K);
+    const int nsl = clen / 4;  // whole slots in this chunk
+    for (int t0 = 0; t0 < nsl; t0 += M) {
+        const int mt = nsl - t0 < M ? nsl - t0 : M;
+        // gather: gradients into the tile; workers and center in registers
+        {
+            u4 v[R];
+            bool ok[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int q = threadIdx.x + r * 256;
+                const int kk = q / M, jl = q % M;
+                ok[r] = kk < K && jl < mt;
+                if (!ok[r]) continue;
+                const int jr = 4 * (t0 + jl);
+                int s = find(jr);
+                if (jr + 4 <= rel(s + 1)) {
+                    v[r] = load_bytes<SB>(gbase(kk, s) + static_cast<uintptr_t>(jr) * ES);
+                } else {  // the slot spans tensors
+                    T e4[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        while (jr + e >= rel(s + 1)) ++s;
+                        e4[e] = reinterpret_cast<const T*>(gbase(kk, s))[jr + e];
+                    }
+                    v[r] = u4{0u, 0u, 0u, 0u};
+                    __builtin_memcpy(&v[r], e4, SB);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                if (!ok[r]) continue;
+                const int q = threadIdx.x + r * 256;
+                if constexpr (SB == 16) *reinterpret_cast<u4*>(gtile(q % M, q / M)) = v[r];
+                else *reinterpret_cast<u2*>(gtile(q % M, q / M)) = u2{v[r].x, v[r].y};
+            }
+        }
+        f4 xv[R], cv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int jl = (threadIdx.x + r * 256) / P;
+            const int64_t J = slot0 + t0 + jl;
+            cv[r] = jl < mt ? load_slot(a.xc, J) : f4(0.0f);
+            xv[r] = jl < mt && i < K ? load_slot(a.x, J * K + i) : f4(0.0f);
+        }
+        __syncthreads();
+        // step, in tensor order
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int jl = (threadIdx.x + r * 256) / P;
+            const int64_t J = slot0 + t0 + jl;
+            const bool slot = jl < mt, live = slot && i < K;
+            u4 raw = u4{0u, 0u, 0u, 0u};
+            if (live) {
+                if constexpr (SB == 16) raw = *reinterpret_cast<const u4*>(gtile(jl, i));
+                else {
+                    const u2 w = *reinterpret_cast<const u2*>(gtile(jl, i));
+                    raw = u4{w.x, w.y, 0u, 0u};
+                }
+                if constexpr (WG) store_bytes<SB>(reinterpret_cast<uintptr_t>(a.gt) + static_cast<uintptr_t>((J * K + i) * SB), raw);
+            }
+            const f4 g = widen_piece(raw, ES);
+            const f4 d = live ? xv[r] - cv[r] : f4(0.0f);
+            xv[r] = fma4(neg_eta, fma4(rho, d, g), xv[r]);
+            if constexpr (P >= 4) {
+                // lanes 0-3 of the slot's group hold one component each
+                const float gs = split_group_sum<P>(g, threadIdx.x) / kf;  // correctly rounded
+                const float ds = split_group_sum<P>(d, threadIdx.x);
+                const int cp = comp_of_lane(i);
+                if (slot && i < 4) {
+                    __builtin_nontemporal_store(gs, a.gbar + J * 4 + cp);
+                    __builtin_nontemporal_store(__builtin_fmaf(a.a, ds, comp(cv[r], cp)), a.xc + J * 4 + cp);
+                }
+            } else {
+                const f4 gs = group_sum4<P>(g) / f4(kf);
+                const f4 cn = fma4(alpha, group_sum4<P>(d), cv[r]);
+                if (slot && i == 0) {
+                    store_slot(a.gbar, J, gs);
+                    store_slot(a.xc, J, cn);
+                }
+            }
+            if (live) store_slot(a.x, J * K + i, xv[r]);
+        }
+        if constexpr (ROWG != ROWX) __syncthreads();  // the gradient pieces are read
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int jl = (threadIdx.x + r * 256) / P;
+            if (jl < mt && i < K) *reinterpret_cast<f4*>(xtile(jl, i)) = xv[r];
+        }
+        __syncthreads();
+        // scatter: lanes walk consecutive slots of one copy's parameters
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int q = threadIdx.x + r * 256;
+            const int kk = q / M, jl = q % M;
+            if (kk >= K || jl >= mt) continue;
+            const int js = t0 + jl, jr = 4 * js;
+            int s = find(jr);
+            const int32_t r1 = rel(s + 1);
+            const float* src = reinterpret_cast<const float*>(xtile(jl, kk));
+            if (jr + 4 <= r1) {
+                const uintptr_t w = xbase(kk, s) + static_cast<uintptr_t>(jr) * 4;
+                if ((w & 15) == 0) {
+                    __builtin_nontemporal_store(*reinterpret_cast<const u4*>(src), reinterpret_cast<u4*>(w));
+                } else {
+                    // whole slots of this tensor in this tile: [run_lo, run_hi)
+                    const int rl = (rel(s) + 3) / 4, rh = r1 / 4;
+                    const int run_lo = rl > t0 ? rl : t0, run_hi = rh < t0 + mt ? rh : t0 + mt;
+                    const uintptr_t G = (w + 15) & ~uintptr_t(15);
+                    const uint32_t sh = static_cast<uint32_t>(G - w);  // bytes of this slot before G
+                    if (js == run_lo)  // bytes before the first granule
+                        for (uint32_t e = 0; e < sh / 4; ++e) reinterpret_cast<float*>(w)[e] = src[e];
+                    if (js + 1 < run_hi) {
+                        const u4 next = *reinterpret_cast<const u4*>(xtile(jl + 1, kk));
+                        __builtin_nontemporal_store(funnel(*reinterpret_cast<const u4*>(src), next, sh),
+                                                    reinterpret_cast<u4*>(G));
+                    } else {  // the run's last slot: bytes after G
+                        for (uint32_t e = sh / 4; e < 4; ++e) reinterpret_cast<float*>(w)[e] = src[e];
+                    }
+                }
+            } else {  // the slot spans tensors
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    while (jr + e >= rel(s + 1)) ++s;
+                    reinterpret_cast<float*>(xbase(kk, s))[jr + e] = src[e];
+                }
+            }
+        }
+        __syncthreads();  // the tile is reused
+    }
+    // the group's last, partial slot: one lane per element, all K copies
+    const int rem = clen - 4 * nsl;
+    if (threadIdx.x < rem) {
+        const int e = threadIdx.x, je = 4 * nsl + e;
+        const int64_t J = slot0 + nsl;
+        int s = find(je);
+        while (je >= rel(s + 1)) ++s;
+        const float c = a.xc[cstart + je];
+        float gv[P], dv[P];
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            gv[q] = 0.0f;
+            dv[q] = 0.0f;
+            if (q >= K) continue;
+            const T graw = reinterpret_cast<const T*>(gbase(q, s))[je];
+            if constexpr (WG) reinterpret_cast<T*>(a.gt)[(J * K + q) * 4 + e] = graw;
+            gv[q] = ES == 4 ? __uint_as_float(static_cast<uint32_t>(graw)) : bf16_to_f32(static_cast<uint16_t>(graw));
+            float* xp = a.x + (J * K + q) * 4 + e;
+            const float xo = *xp;
+            dv[q] = xo - c;
+            const float xn = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, dv[q], gv[q]), xo);
+            *xp = xn;
+            reinterpret_cast<float*>(xbase(q, s))[je] = xn;
+        }
+        a.gbar[cstart + je] = Tree<P>::sum(gv) / kf;
+        a.xc[cstart + je] = __builtin_fmaf(a.a, Tree<P>::sum(dv), c);
+    }
+}
+
 // ---------------------------------------------------------- launching
 
 // Slots per lane: enough that a wave's single-stream output covers a
@@ -726,6 +988,30 @@ hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack
     switch (next_pow2(tl->K)) {
 #define TC_CASE(p) \
     case p: return run_tpack<p>(a, tl->elem, unpack, blocks, stream);
+        TC_FOR_P(TC_CASE)
+#undef TC_CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <int P, typename T>
+hipError_t run_tpipe(const TPipeArgs& a, unsigned blocks, hipStream_t stream) {
+    dim3 grid(blocks);
+    if (a.gt) hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, true>), grid, dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, false>), grid, dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_tensor_pipeline(const tc_tensorlist* grads, const tc_tensorlist* params, void* gt, float* gbar,
+                                  float* x, float* xc, float eta, float rho, hipStream_t stream) {
+    const tc_group* g = grads->g;
+    TPipeArgs a{g->d_offsets, g->d_chunk_first, grads->d_ptrs, params->d_ptrs, gt, gbar, x, xc,
+                g->n, grads->K, g->N, g->chunk, eta, rho, eta * rho};
+    const unsigned blocks = static_cast<unsigned>(g->nchunks);
+    const bool bf16 = grads->elem == 2;
+    switch (next_pow2(grads->K)) {
+#define TC_CASE(p) \
+    case p: return bf16 ? run_tpipe<p, uint16_t>(a, blocks, stream) : run_tpipe<p, uint32_t>(a, blocks, stream);
         TC_FOR_P(TC_CASE)
 #undef TC_CASE
         default: return hipErrorInvalidValue;
