@@ -33,6 +33,29 @@ namespace tc {
 // tables instead.
 constexpr int kMaxStage = 1024;
 
+// Device access to global memory at an address held as an integer (pointers
+// read from the tensor lists' tables, addresses formed by arithmetic).  The
+// address space is stated so that the compiler emits global, not flat,
+// instructions: a flat access also counts against the LDS wait counter, so
+// every later wait for an LDS access would wait for it as well.
+#define TC_GLOBAL __attribute__((address_space(1)))
+template <typename V>
+__device__ __forceinline__ V gld(uintptr_t a) {
+    return *reinterpret_cast<const TC_GLOBAL V*>(a);
+}
+template <typename V>
+__device__ __forceinline__ V gld_nt(uintptr_t a) {
+    return __builtin_nontemporal_load(reinterpret_cast<const TC_GLOBAL V*>(a));
+}
+template <typename V>
+__device__ __forceinline__ void gst(uintptr_t a, V v) {
+    *reinterpret_cast<TC_GLOBAL V*>(a) = v;
+}
+template <typename V>
+__device__ __forceinline__ void gst_nt(uintptr_t a, V v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<TC_GLOBAL V*>(a));
+}
+
 // Records a printf-style message as this thread's last error.
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();

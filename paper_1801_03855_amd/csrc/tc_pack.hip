@@ -106,9 +106,9 @@ __device__ __forceinline__ bool whole(const SegView& v, uintptr_t A) { return A 
 // The 16 source bytes of a whole granule.
 __device__ __forceinline__ u4 load_granule(const SegView& v, uintptr_t A) {
     const uintptr_t S = A + v.delta;
-    if ((S & 15) == 0) return __builtin_nontemporal_load(reinterpret_cast<const u4*>(S));
-    const u4* g = reinterpret_cast<const u4*>(S & ~uintptr_t(15));
-    return funnel(g[0], g[1], static_cast<uint32_t>(S & 15));
+    if ((S & 15) == 0) return gld_nt<u4>(S);
+    const uintptr_t g = S & ~uintptr_t(15);
+    return funnel(gld<u4>(g), gld<u4>(g + 16), static_cast<uint32_t>(S & 15));
 }
 
 // Element-by-element copy of the part of granule A inside segment v.
@@ -118,7 +118,7 @@ __device__ __forceinline__ void copy_partial(const SegView& v, uintptr_t A) {
     const uintptr_t lo = A > v.d0 ? A : v.d0;
     const uintptr_t hi = A + 16 < v.d1 ? A + 16 : v.d1;
     for (uintptr_t x = lo; x < hi; x += es)
-        *reinterpret_cast<T*>(x) = *reinterpret_cast<const T*>(x + v.delta);
+        gst<T>(x, gld<T>(x + v.delta));
 }
 
 // Element-by-element copy of a chunk whose segments stay in global memory.
@@ -131,9 +131,10 @@ __device__ void copy_chunk_global(const int64_t* off, void* const* cp, int nseg,
             const int mid = (lo + hi + 1) >> 1;
             if (clamp_rel(off[mid] - cstart, clen) <= jr) lo = mid; else hi = mid - 1;
         }
-        T* te = static_cast<T*>(cp[lo]) + (cstart + jr - off[lo]);
-        if (UNPACK) *te = flat_chunk[jr];
-        else flat_chunk[jr] = *te;
+        const uintptr_t te = reinterpret_cast<uintptr_t>(cp[lo]) + static_cast<uintptr_t>((cstart + jr - off[lo]) * sizeof(T));
+        const uintptr_t tf = reinterpret_cast<uintptr_t>(flat_chunk + jr);
+        if (UNPACK) gst<T>(te, gld<T>(tf));
+        else gst<T>(tf, gld<T>(te));
     }
 }
 
@@ -229,7 +230,7 @@ __global__ __launch_bounds__(TC_PACK_THREADS) void pack_kernel(PackKernelArgs a)
         }
 #pragma unroll
         for (int i = 0; i < B; ++i)
-            if (full[i]) __builtin_nontemporal_store(val[i], reinterpret_cast<u4*>(A[i]));
+            if (full[i]) gst_nt<u4>(A[i], val[i]);
 #pragma unroll
         for (int i = 0; i < B; ++i)
             if (!full[i] && q0 + i * TC_PACK_THREADS < total) copy_partial<T>(v[i], A[i]);

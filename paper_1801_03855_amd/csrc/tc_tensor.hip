@@ -411,21 +411,21 @@ __device__ __forceinline__ u4 funnel(u4 lo, u4 hi, uint32_t sh) {
 template <int SB>
 __device__ __forceinline__ u4 load_bytes(uintptr_t S) {
     if ((S & (SB - 1)) == 0) {
-        if constexpr (SB == 16) return __builtin_nontemporal_load(reinterpret_cast<const u4*>(S));
-        const u2 w = __builtin_nontemporal_load(reinterpret_cast<const u2*>(S));
+        if constexpr (SB == 16) return gld_nt<u4>(S);
+        const u2 w = gld_nt<u2>(S);
         return u4{w.x, w.y, 0u, 0u};
     }
-    const u4* g = reinterpret_cast<const u4*>(S & ~uintptr_t(15));
+    const uintptr_t g = S & ~uintptr_t(15);
     const uint32_t sh = static_cast<uint32_t>(S & 15);
-    const u4 g0 = g[0];
-    const u4 g1 = sh + SB > 16 ? g[1] : g0;
+    const u4 g0 = gld<u4>(g);
+    const u4 g1 = sh + SB > 16 ? gld<u4>(g + 16) : g0;
     return funnel(g0, g1, sh);
 }
 
 template <int SB>
 __device__ __forceinline__ void store_bytes(uintptr_t D, u4 v) {
-    if constexpr (SB == 16) __builtin_nontemporal_store(v, reinterpret_cast<u4*>(D));
-    else __builtin_nontemporal_store(u2{v.x, v.y}, reinterpret_cast<u2*>(D));
+    if constexpr (SB == 16) gst_nt<u4>(D, v);
+    else gst_nt<u2>(D, u2{v.x, v.y});
 }
 
 // Workgroup b moves chunk b of all K copies through LDS, M slots at a time
@@ -518,7 +518,7 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         while (jr + e >= rel(s + 1)) ++s;
-                        e4[e] = reinterpret_cast<const T*>(base(kk, s))[jr + e];
+                        e4[e] = gld<T>(base(kk, s) + static_cast<uintptr_t>(jr + e) * ES);
                     }
                     v[r] = u4{0u, 0u, 0u, 0u};
                     __builtin_memcpy(&v[r], e4, SB);
@@ -538,12 +538,8 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                 const int q = threadIdx.x + r * 256;
                 const int jl = q / P, kk = q % P;
                 if (kk >= K || jl >= mt) continue;
-                if constexpr (SB == 16)
-                    __builtin_nontemporal_store(*reinterpret_cast<const u4*>(tile(jl, kk)),
-                                                reinterpret_cast<u4*>(piece(t0 + jl, kk)));
-                else
-                    __builtin_nontemporal_store(*reinterpret_cast<const u2*>(tile(jl, kk)),
-                                                reinterpret_cast<u2*>(piece(t0 + jl, kk)));
+                if constexpr (SB == 16) gst_nt<u4>(piece(t0 + jl, kk), *reinterpret_cast<const u4*>(tile(jl, kk)));
+                else gst_nt<u2>(piece(t0 + jl, kk), *reinterpret_cast<const u2*>(tile(jl, kk)));
             }
         } else {
             // tensor -> tile, in tensor order
@@ -554,9 +550,9 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                 const int jl = q / P, kk = q % P;
                 if (kk >= K || jl >= mt) continue;
                 if constexpr (SB == 16) {
-                    v[r] = __builtin_nontemporal_load(reinterpret_cast<const u4*>(piece(t0 + jl, kk)));
+                    v[r] = gld_nt<u4>(piece(t0 + jl, kk));
                 } else {
-                    const u2 w = __builtin_nontemporal_load(reinterpret_cast<const u2*>(piece(t0 + jl, kk)));
+                    const u2 w = gld_nt<u2>(piece(t0 + jl, kk));
                     v[r] = u4{w.x, w.y, 0u, 0u};
                 }
             }
@@ -582,33 +578,30 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                 if (jr + 4 <= r1) {
                     const uintptr_t w = base(kk, s) + static_cast<uintptr_t>(jr) * ES;
                     if ((w & (SB - 1)) == 0) {
-                        if constexpr (SB == 16)
-                            __builtin_nontemporal_store(*reinterpret_cast<const u4*>(src), reinterpret_cast<u4*>(w));
-                        else
-                            __builtin_nontemporal_store(*reinterpret_cast<const u2*>(src), reinterpret_cast<u2*>(w));
+                        if constexpr (SB == 16) gst_nt<u4>(w, *reinterpret_cast<const u4*>(src));
+                        else gst_nt<u2>(w, *reinterpret_cast<const u2*>(src));
                     } else if constexpr (SB == 16) {
                         const uintptr_t G = (w + 15) & ~uintptr_t(15);
                         const uint32_t sh = static_cast<uint32_t>(G - w);  // bytes of this slot before G
                         const int run_lo = (rel(s) + 3) / 4, run_hi = r1 / 4;  // whole slots of this tensor here
                         if (js == run_lo)  // bytes before the first granule
-                            for (uint32_t e = 0; e < sh / ES; ++e) reinterpret_cast<T*>(w)[e] = src[e];
+                            for (uint32_t e = 0; e < sh / ES; ++e) gst<T>(w + e * ES, src[e]);
                         if (js + 1 < run_hi) {
                             const u4 next = jl + 1 < mt ? *reinterpret_cast<const u4*>(tile(jl + 1, kk))
                                                         : load_bytes<SB>(piece(js + 1, kk));
-                            __builtin_nontemporal_store(funnel(*reinterpret_cast<const u4*>(src), next, sh),
-                                                        reinterpret_cast<u4*>(G));
+                            gst_nt<u4>(G, funnel(*reinterpret_cast<const u4*>(src), next, sh));
                         } else {  // the last whole slot: bytes after G
-                            for (uint32_t e = sh / ES; e < 4; ++e) reinterpret_cast<T*>(w)[e] = src[e];
+                            for (uint32_t e = sh / ES; e < 4; ++e) gst<T>(w + e * ES, src[e]);
                         }
                     } else {
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) reinterpret_cast<T*>(w)[e] = src[e];
+                        for (int e = 0; e < 4; ++e) gst<T>(w + e * ES, src[e]);
                     }
                 } else {  // the slot spans tensors
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         while (jr + e >= rel(s + 1)) ++s;
-                        reinterpret_cast<T*>(base(kk, s))[jr + e] = src[e];
+                        gst<T>(base(kk, s) + static_cast<uintptr_t>(jr + e) * ES, src[e]);
                     }
                 }
             }
@@ -622,10 +615,10 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
         const int je = 4 * nsl + e;
         int s = find(je);
         while (je >= rel(s + 1)) ++s;
-        T* t = reinterpret_cast<T*>(base(kk, s)) + je;
-        T* pc = reinterpret_cast<T*>(tens) + ((slot0 + nsl) * K + kk) * 4 + e;
-        if (UNPACK) *t = *pc;
-        else *pc = *t;
+        const uintptr_t t = base(kk, s) + static_cast<uintptr_t>(je) * ES;
+        const uintptr_t pc = tens + static_cast<uintptr_t>((((slot0 + nsl) * K + kk) * 4 + e) * ES);
+        if (UNPACK) gst<T>(t, gld<T>(pc));
+        else gst<T>(pc, gld<T>(t));
     }
 }
 
@@ -672,6 +665,13 @@ struct TPipeArgs {
 
 constexpr int kPipeStage = 512;
 
+// Pieces (slot of one copy) per LDS tile: 256 lanes move TC_PIPE_TILE/256
+// pieces each per phase.
+#ifndef TC_PIPE_TILE
+#define TC_PIPE_TILE 1024
+#endif
+
+
 __device__ __forceinline__ f4 widen_piece(u4 v, int es) {
     if (es == 4) return f4{__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w)};
     return f4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
@@ -680,12 +680,12 @@ __device__ __forceinline__ f4 widen_piece(u4 v, int es) {
 
 __device__ __forceinline__ float comp(f4 v, int c) { return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w; }
 
-template <int P, typename T, bool WG>
+template <int P, typename T, bool WG, typename I>
 __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
     constexpr int ES = sizeof(T);
     constexpr int SB = 4 * ES;                         // gradient slot bytes
-    constexpr int M = 1024 / P > 16 ? 1024 / P : 16;   // slots per tile
-    constexpr int R = (M * P) / 256;                   // pieces per lane and phase
+    constexpr int M = TC_PIPE_TILE / P > 16 ? TC_PIPE_TILE / P : 16;  // slots per tile
+    constexpr int R = (M * P) / 256;                                 // pieces per lane and phase
     constexpr int ROWG = (P + 1) * SB, ROWX = (P + 1) * 16;
     __shared__ int32_t s_rel[kPipeStage + 1];
     __shared__ uintptr_t s_gbase[kPipeStage];
@@ -755,7 +755,7 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         while (jr + e >= rel(s + 1)) ++s;
-                        e4[e] = reinterpret_cast<const T*>(gbase(kk, s))[jr + e];
+                        e4[e] = gld<T>(gbase(kk, s) + static_cast<uintptr_t>(jr + e) * ES);
                     }
                     v[r] = u4{0u, 0u, 0u, 0u};
                     __builtin_memcpy(&v[r], e4, SB);
@@ -773,16 +773,16 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int jl = (threadIdx.x + r * 256) / P;
-            const int64_t J = slot0 + t0 + jl;
+            const I J = static_cast<I>(slot0 + t0 + jl);
             cv[r] = jl < mt ? load_slot(a.xc, J) : f4(0.0f);
-            xv[r] = jl < mt && i < K ? load_slot(a.x, J * K + i) : f4(0.0f);
+            xv[r] = jl < mt && i < K ? load_slot(a.x, J * I(K) + I(i)) : f4(0.0f);
         }
         __syncthreads();
         // step, in tensor order
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int jl = (threadIdx.x + r * 256) / P;
-            const int64_t J = slot0 + t0 + jl;
+            const I J = static_cast<I>(slot0 + t0 + jl);
             const bool slot = jl < mt, live = slot && i < K;
             u4 raw = u4{0u, 0u, 0u, 0u};
             if (live) {
@@ -791,7 +791,7 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
                     const u2 w = *reinterpret_cast<const u2*>(gtile(jl, i));
                     raw = u4{w.x, w.y, 0u, 0u};
                 }
-                if constexpr (WG) store_bytes<SB>(reinterpret_cast<uintptr_t>(a.gt) + static_cast<uintptr_t>((J * K + i) * SB), raw);
+                if constexpr (WG) store_bytes<SB>(reinterpret_cast<uintptr_t>(a.gt) + (J * I(K) + I(i)) * I(SB), raw);
             }
             const f4 g = widen_piece(raw, ES);
             const f4 d = live ? xv[r] - cv[r] : f4(0.0f);
@@ -802,8 +802,8 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
                 const float ds = split_group_sum<P>(d, threadIdx.x);
                 const int cp = comp_of_lane(i);
                 if (slot && i < 4) {
-                    __builtin_nontemporal_store(gs, a.gbar + J * 4 + cp);
-                    __builtin_nontemporal_store(__builtin_fmaf(a.a, ds, comp(cv[r], cp)), a.xc + J * 4 + cp);
+                    __builtin_nontemporal_store(gs, a.gbar + (J * I(4) + I(cp)));
+                    __builtin_nontemporal_store(__builtin_fmaf(a.a, ds, comp(cv[r], cp)), a.xc + (J * I(4) + I(cp)));
                 }
             } else {
                 const f4 gs = group_sum4<P>(g) / f4(kf);
@@ -813,7 +813,7 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
                     store_slot(a.xc, J, cn);
                 }
             }
-            if (live) store_slot(a.x, J * K + i, xv[r]);
+            if (live) store_slot(a.x, J * I(K) + I(i), xv[r]);
         }
         if constexpr (ROWG != ROWX) __syncthreads();  // the gradient pieces are read
 #pragma unroll
@@ -835,7 +835,7 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
             if (jr + 4 <= r1) {
                 const uintptr_t w = xbase(kk, s) + static_cast<uintptr_t>(jr) * 4;
                 if ((w & 15) == 0) {
-                    __builtin_nontemporal_store(*reinterpret_cast<const u4*>(src), reinterpret_cast<u4*>(w));
+                    gst_nt<u4>(w, *reinterpret_cast<const u4*>(src));
                 } else {
                     // whole slots of this tensor in this tile: [run_lo, run_hi)
                     const int rl = (rel(s) + 3) / 4, rh = r1 / 4;
@@ -843,20 +843,19 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
                     const uintptr_t G = (w + 15) & ~uintptr_t(15);
                     const uint32_t sh = static_cast<uint32_t>(G - w);  // bytes of this slot before G
                     if (js == run_lo)  // bytes before the first granule
-                        for (uint32_t e = 0; e < sh / 4; ++e) reinterpret_cast<float*>(w)[e] = src[e];
+                        for (uint32_t e = 0; e < sh / 4; ++e) gst<float>(w + e * 4, src[e]);
                     if (js + 1 < run_hi) {
                         const u4 next = *reinterpret_cast<const u4*>(xtile(jl + 1, kk));
-                        __builtin_nontemporal_store(funnel(*reinterpret_cast<const u4*>(src), next, sh),
-                                                    reinterpret_cast<u4*>(G));
+                        gst_nt<u4>(G, funnel(*reinterpret_cast<const u4*>(src), next, sh));
                     } else {  // the run's last slot: bytes after G
-                        for (uint32_t e = sh / 4; e < 4; ++e) reinterpret_cast<float*>(w)[e] = src[e];
+                        for (uint32_t e = sh / 4; e < 4; ++e) gst<float>(w + e * 4, src[e]);
                     }
                 }
             } else {  // the slot spans tensors
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     while (jr + e >= rel(s + 1)) ++s;
-                    reinterpret_cast<float*>(xbase(kk, s))[jr + e] = src[e];
+                    gst<float>(xbase(kk, s) + static_cast<uintptr_t>(jr + e) * 4, src[e]);
                 }
             }
         }
@@ -876,15 +875,15 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
             gv[q] = 0.0f;
             dv[q] = 0.0f;
             if (q >= K) continue;
-            const T graw = reinterpret_cast<const T*>(gbase(q, s))[je];
-            if constexpr (WG) reinterpret_cast<T*>(a.gt)[(J * K + q) * 4 + e] = graw;
+            const T graw = gld<T>(gbase(q, s) + static_cast<uintptr_t>(je) * ES);
+            if constexpr (WG) gst<T>(reinterpret_cast<uintptr_t>(a.gt) + static_cast<uintptr_t>(((J * K + q) * 4 + e) * ES), graw);
             gv[q] = ES == 4 ? __uint_as_float(static_cast<uint32_t>(graw)) : bf16_to_f32(static_cast<uint16_t>(graw));
             float* xp = a.x + (J * K + q) * 4 + e;
             const float xo = *xp;
             dv[q] = xo - c;
             const float xn = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, dv[q], gv[q]), xo);
             *xp = xn;
-            reinterpret_cast<float*>(xbase(q, s))[je] = xn;
+            gst<float>(xbase(q, s) + static_cast<uintptr_t>(je) * 4, xn);
         }
         a.gbar[cstart + je] = Tree<P>::sum(gv) / kf;
         a.xc[cstart + je] = __builtin_fmaf(a.a, Tree<P>::sum(dv), c);
@@ -997,8 +996,14 @@ hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack
 template <int P, typename T>
 hipError_t run_tpipe(const TPipeArgs& a, unsigned blocks, hipStream_t stream) {
     dim3 grid(blocks);
-    if (a.gt) hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, true>), grid, dim3(256), 0, stream, a);
-    else hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, false>), grid, dim3(256), 0, stream, a);
+    const int64_t nslot = a.N / 4;
+    if ((nslot + 1) * a.K * 16 < (int64_t(1) << 32)) {
+        if (a.gt) hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, true, uint32_t>), grid, dim3(256), 0, stream, a);
+        else hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, false, uint32_t>), grid, dim3(256), 0, stream, a);
+    } else {
+        if (a.gt) hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, true, int64_t>), grid, dim3(256), 0, stream, a);
+        else hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, false, int64_t>), grid, dim3(256), 0, stream, a);
+    }
     return hipGetLastError();
 }
 
