@@ -222,6 +222,34 @@ def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
     return {"step_ms": step_ms, "per_op_ms": per_op_ms}
 
 
+def copy_ceiling(tc, reps: int = 20) -> dict:
+    """Plain device-to-device copies of 1 GiB (read + write bytes over the
+    time): torch's copy_ and the library's 16-byte vector copy (tc_broadcast
+    into one copy); the faster is what this machine's HBM gives the simplest
+    stream."""
+    import torch
+
+    src = torch.ones(256 << 20, device="cuda")
+    dst = torch.empty_like(src)
+    one = tc.Group([src.numel()])
+    out = {}
+    for name, fn in (("torch copy_", lambda: dst.copy_(src)), ("tc_broadcast, K = 1", lambda: tc.broadcast(one, src, [dst]))):
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        out[name] = round(2 * (1 << 30) / (a.elapsed_time(b) / reps * 1e-3) / 1e9, 1)
+    del src, dst
+    torch.cuda.empty_cache()
+    best = max(out, key=out.get)
+    return {"GB/s": out[best], "by": best, "all": out, "what": "1 GiB device-to-device copy, read + write bytes"}
+
+
 def fused_bytes(K: int, N: int, s_g: int, write_g: bool = True) -> int:
     """Algorithmic bytes of the one-pass pipeline: read the K gradient
     lists, the K workers and the center; write the packed gradients (when
@@ -398,6 +426,9 @@ def main():
     roof = {"bound": "hbm", "kernel": f"{dom} ({first} layout)", "achieved": kernels[dom]["GB/s"],
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels[dom]["frac"], "traffic": traffic,
             "algorithmic_bytes": kernels[dom]["bytes"], "avg_ms": kernels[dom]["ms"]}
+    copy = copy_ceiling(tc)
+    roof["copy_ceiling"] = copy
+    roof["frac_of_copy_ceiling"] = round(kernels[dom]["GB/s"] / copy["GB/s"], 4)
     layouts = {}
     for lay, r in results.items():
         layouts[lay] = {"value": round(step_bytes / (r["step_ms"] * 1e-3) / 1e9, 2), "ms_per_step": round(r["step_ms"], 5),
@@ -413,7 +444,9 @@ def main():
             gbs = b / (ft[write_g] * 1e-3) / 1e9
             fused[key] = {"ms_per_step": round(ft[write_g], 5), "steps_per_s": round(1e3 / ft[write_g], 2),
                           "algorithmic_bytes": b, "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
-                          "speedup_vs_four_calls": round(four_ms / ft[write_g], 3) if four_ms else None}
+                          "speedup_vs_four_calls": round(four_ms / ft[write_g], 3) if four_ms else None,
+                          "traffic": recorded_traffic(args.workload, "tensor").get(
+                              "pipeline" if write_g else "pipeline_no_g")}
 
     extra = None
     if not args.no_next_rows and args.workload == "resnet50_k8_pipeline":
