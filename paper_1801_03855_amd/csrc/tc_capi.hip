@@ -97,6 +97,9 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         return static_cast<int32_t>(it - g->offsets.begin()) - 1;
     };
     for (int64_t b = 0; b < g->nchunks; ++b) g->chunk_first[b] = tensor_at(b * g->chunk);
+    g->slot_bounds = true;
+    for (int32_t t = 1; t < n; ++t)
+        if (g->offsets[t] % 4 != 0 && g->offsets[t] < g->N / 4 * 4) g->slot_bounds = false;
     g->chunk_first[g->nchunks] = g->N > 0 ? tensor_at(g->N - 1) : 0;
 
     hipError_t e = hipGetDevice(&g->device);
@@ -159,6 +162,10 @@ TC_API tc_tensorlist* tc_tensorlist_create(const tc_group* g, int32_t K, const v
     tl->dtype = dtype;
     tl->elem = es;
     tl->ptrs.assign(ptrs, ptrs + static_cast<int64_t>(K) * g->n);
+    uintptr_t bits = 0;
+    for (int64_t q = 0; q < static_cast<int64_t>(tl->ptrs.size()); ++q)
+        if (g->sizes[q % g->n] > 0) bits |= reinterpret_cast<uintptr_t>(tl->ptrs[q]);
+    tl->slot_aligned = (bits & static_cast<uintptr_t>(4 * es - 1)) == 0;
     const size_t bytes = tl->ptrs.size() * sizeof(void*);
     hipError_t e = hipMalloc(&tl->d_ptrs, bytes);
     if (e != hipSuccess) { hip_fail(e, "hipMalloc (pointer table)"); delete tl; return nullptr; }

@@ -107,6 +107,8 @@ struct tc_group {
     int64_t chunk = 0;                 // elements per pack/unpack chunk
     int64_t nchunks = 0;               // ceil(N / chunk)
     std::vector<int32_t> chunk_first;  // nchunks + 1
+    bool slot_bounds = false;          // every tensor boundary before the last,
+                                       // partial slot is a multiple of 4
     int64_t* d_offsets = nullptr;
     int32_t* d_chunk_first = nullptr;
 };
@@ -119,5 +121,6 @@ struct tc_tensorlist {
     int32_t dtype = TC_F32;
     int32_t elem = 4;
     std::vector<const void*> ptrs;
+    bool slot_aligned = false;  // every non-empty tensor starts on a 4-element boundary
     void** d_ptrs = nullptr;
 };

@@ -448,11 +448,16 @@ __device__ __forceinline__ void store_bytes(uintptr_t D, u4 v) {
 //           last one the bytes after it (binary32; an unaligned bfloat16
 //           slot is stored element by element).
 // A slot spanning two tensors moves element by element.
+// Pieces (one slot of one copy) per LDS tile of the pack and unpack.
+#ifndef TC_TPACK_TILE
+#define TC_TPACK_TILE 1024
+#endif
+
 template <int P, typename T, bool UNPACK>
 __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
     constexpr int ES = sizeof(T);
     constexpr int SB = 4 * ES;                      // slot bytes
-    constexpr int M = 1024 / P > 16 ? 1024 / P : 16;  // slots per LDS tile
+    constexpr int M = TC_TPACK_TILE / P > 16 ? TC_TPACK_TILE / P : 16;  // slots per LDS tile
     constexpr int ROW = (P + 1) * SB;               // padded tile row, bytes
     __shared__ int32_t s_rel[kMaxStage + 1];
     __shared__ uintptr_t s_base[kMaxStage];
@@ -680,7 +685,7 @@ __device__ __forceinline__ f4 widen_piece(u4 v, int es) {
 
 __device__ __forceinline__ float comp(f4 v, int c) { return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w; }
 
-template <int P, typename T, bool WG, typename I>
+template <int P, typename T, bool WG, typename I, bool DIRECT>
 __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
     constexpr int ES = sizeof(T);
     constexpr int SB = 4 * ES;                         // gradient slot bytes
@@ -705,6 +710,7 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
         return reinterpret_cast<uintptr_t>(ptrs[static_cast<int64_t>(kk) * a.n + lo + s]) -
                static_cast<uintptr_t>((a.offsets[lo + s] - cstart) * es);
     };
+    const int nsl = clen / 4;  // whole slots in this chunk
     if (rel_staged)
         for (int s = threadIdx.x; s <= nseg; s += 256) s_rel[s] = rel_global(s);
     if (base_staged)
@@ -733,8 +739,70 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
     const int64_t slot0 = cstart / 4;
     const f4 rho = f4(a.rho), neg_eta = f4(-a.eta), alpha = f4(a.a);
     const float kf = static_cast<float>(K);
-    const int nsl = clen / 4;  // whole slots in this chunk
-    for (int t0 = 0; t0 < nsl; t0 += M) {
+    // The step on one piece (slot J of worker i): the packed gradient out,
+    // the AVG and the center from the split butterflies, the new worker out
+    // and returned.  Every lane calls it (the butterflies need all lanes).
+    auto step = [&](I J, bool slot, bool live, u4 raw, f4 x, f4 c) -> f4 {
+        if constexpr (WG)
+            if (live) store_bytes<SB>(reinterpret_cast<uintptr_t>(a.gt) + (J * I(K) + I(i)) * I(SB), raw);
+        const f4 g = widen_piece(raw, ES);
+        const f4 d = live ? x - c : f4(0.0f);
+        const f4 xn = fma4(neg_eta, fma4(rho, d, g), x);
+        if constexpr (P >= 4) {
+            // lanes 0-3 of the slot's group hold one component each
+            const float gs = split_group_sum<P>(g, threadIdx.x) / kf;  // correctly rounded
+            const float ds = split_group_sum<P>(d, threadIdx.x);
+            const int cp = comp_of_lane(i);
+            if (slot && i < 4) {
+                __builtin_nontemporal_store(gs, a.gbar + (J * I(4) + I(cp)));
+                __builtin_nontemporal_store(__builtin_fmaf(a.a, ds, comp(c, cp)), a.xc + (J * I(4) + I(cp)));
+            }
+        } else {
+            const f4 gs = group_sum4<P>(g) / f4(kf);
+            const f4 cn = fma4(alpha, group_sum4<P>(d), c);
+            if (slot && i == 0) {
+                store_slot(a.gbar, J, gs);
+                store_slot(a.xc, J, cn);
+            }
+        }
+        if (live) store_slot(a.x, J * I(K) + I(i), xn);
+        return xn;
+    };
+    if constexpr (DIRECT) {
+        // every whole slot lies inside one tensor and every tensor is
+        // slot-aligned in every copy: the chunk moves straight between
+        // registers and the per-layer tensors, without the tiles
+        for (int t0 = 0; t0 < nsl; t0 += M) {
+            const int mt = nsl - t0 < M ? nsl - t0 : M;
+            f4 xv[R], cv[R];
+            u4 gr[R];
+            int seg[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int jl = (threadIdx.x + r * 256) / P;
+                const I J = static_cast<I>(slot0 + t0 + jl);
+                const bool live = jl < mt && i < K;
+                cv[r] = jl < mt ? load_slot(a.xc, J) : f4(0.0f);
+                xv[r] = live ? load_slot(a.x, J * I(K) + I(i)) : f4(0.0f);
+                gr[r] = u4{0u, 0u, 0u, 0u};
+                seg[r] = 0;
+                if (live) {
+                    const int jr = 4 * (t0 + jl);
+                    seg[r] = find(jr);
+                    gr[r] = load_bytes<SB>(gbase(i, seg[r]) + static_cast<uintptr_t>(jr) * ES);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int jl = (threadIdx.x + r * 256) / P;
+                const I J = static_cast<I>(slot0 + t0 + jl);
+                const bool live = jl < mt && i < K;
+                const f4 xn = step(J, jl < mt, live, gr[r], xv[r], cv[r]);
+                if (live) gst_nt<u4>(xbase(i, seg[r]) + static_cast<uintptr_t>(4 * (t0 + jl)) * 4, __builtin_bit_cast(u4, xn));
+            }
+        }
+    }
+    for (int t0 = 0; !DIRECT && t0 < nsl; t0 += M) {
         const int mt = nsl - t0 < M ? nsl - t0 : M;
         // gather: gradients into the tile; workers and center in registers
         {
@@ -791,29 +859,8 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
                     const u2 w = *reinterpret_cast<const u2*>(gtile(jl, i));
                     raw = u4{w.x, w.y, 0u, 0u};
                 }
-                if constexpr (WG) store_bytes<SB>(reinterpret_cast<uintptr_t>(a.gt) + (J * I(K) + I(i)) * I(SB), raw);
             }
-            const f4 g = widen_piece(raw, ES);
-            const f4 d = live ? xv[r] - cv[r] : f4(0.0f);
-            xv[r] = fma4(neg_eta, fma4(rho, d, g), xv[r]);
-            if constexpr (P >= 4) {
-                // lanes 0-3 of the slot's group hold one component each
-                const float gs = split_group_sum<P>(g, threadIdx.x) / kf;  // correctly rounded
-                const float ds = split_group_sum<P>(d, threadIdx.x);
-                const int cp = comp_of_lane(i);
-                if (slot && i < 4) {
-                    __builtin_nontemporal_store(gs, a.gbar + (J * I(4) + I(cp)));
-                    __builtin_nontemporal_store(__builtin_fmaf(a.a, ds, comp(cv[r], cp)), a.xc + (J * I(4) + I(cp)));
-                }
-            } else {
-                const f4 gs = group_sum4<P>(g) / f4(kf);
-                const f4 cn = fma4(alpha, group_sum4<P>(d), cv[r]);
-                if (slot && i == 0) {
-                    store_slot(a.gbar, J, gs);
-                    store_slot(a.xc, J, cn);
-                }
-            }
-            if (live) store_slot(a.x, J * I(K) + I(i), xv[r]);
+            xv[r] = step(J, slot, live, raw, xv[r], cv[r]);
         }
         if constexpr (ROWG != ROWX) __syncthreads();  // the gradient pieces are read
 #pragma unroll
@@ -861,33 +908,46 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
         }
         __syncthreads();  // the tile is reused
     }
-    // the group's last, partial slot: one lane per element, all K copies
-    const int rem = clen - 4 * nsl;
-    if (threadIdx.x < rem) {
-        const int e = threadIdx.x, je = 4 * nsl + e;
-        const int64_t J = slot0 + nsl;
-        int s = find(je);
-        while (je >= rel(s + 1)) ++s;
-        const float c = a.xc[cstart + je];
-        float gv[P], dv[P];
-#pragma unroll
-        for (int q = 0; q < P; ++q) {
-            gv[q] = 0.0f;
-            dv[q] = 0.0f;
-            if (q >= K) continue;
-            const T graw = gld<T>(gbase(q, s) + static_cast<uintptr_t>(je) * ES);
-            if constexpr (WG) gst<T>(reinterpret_cast<uintptr_t>(a.gt) + static_cast<uintptr_t>(((J * K + q) * 4 + e) * ES), graw);
-            gv[q] = ES == 4 ? __uint_as_float(static_cast<uint32_t>(graw)) : bf16_to_f32(static_cast<uint16_t>(graw));
-            float* xp = a.x + (J * K + q) * 4 + e;
-            const float xo = *xp;
-            dv[q] = xo - c;
-            const float xn = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, dv[q], gv[q]), xo);
-            *xp = xn;
-            gst<float>(xbase(q, s) + static_cast<uintptr_t>(je) * 4, xn);
-        }
-        a.gbar[cstart + je] = Tree<P>::sum(gv) / kf;
-        a.xc[cstart + je] = __builtin_fmaf(a.a, Tree<P>::sum(dv), c);
+}
+
+// The group's last, partial slot (N not a multiple of 4) in a launch of its
+// own, one lane per element and all K copies in it, with the arithmetic and
+// summation order of the main kernel (kept apart so that the main kernel's
+// registers are not sized for it).
+template <int P, typename T, bool WG>
+__global__ __launch_bounds__(64) void tensor_pipeline_tail_kernel(TPipeArgs a) {
+    constexpr int ES = sizeof(T);
+    const int64_t nsl = a.N / 4;  // whole slots of the group
+    const int e = threadIdx.x;
+    const int64_t je = 4 * nsl + e;
+    if (je >= a.N) return;
+    int l = 0, h = a.n - 1;  // the last tensor whose start is <= je
+    while (l < h) {
+        const int mid = (l + h + 1) >> 1;
+        if (a.offsets[mid] <= je) l = mid; else h = mid - 1;
     }
+    const int64_t loc = je - a.offsets[l];
+    const int K = a.K;
+    const float c = a.xc[je];
+    float gv[P], dv[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+        gv[q] = 0.0f;
+        dv[q] = 0.0f;
+        if (q >= K) continue;
+        const int64_t tq = static_cast<int64_t>(q) * a.n + l;
+        const T graw = gld<T>(reinterpret_cast<uintptr_t>(a.gptrs[tq]) + static_cast<uintptr_t>(loc) * ES);
+        const int64_t idx = (nsl * K + q) * 4 + e;
+        if constexpr (WG) gst<T>(reinterpret_cast<uintptr_t>(a.gt) + static_cast<uintptr_t>(idx) * ES, graw);
+        gv[q] = ES == 4 ? __uint_as_float(static_cast<uint32_t>(graw)) : bf16_to_f32(static_cast<uint16_t>(graw));
+        const float xo = a.x[idx];
+        dv[q] = xo - c;
+        const float xn = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, dv[q], gv[q]), xo);
+        a.x[idx] = xn;
+        gst<float>(reinterpret_cast<uintptr_t>(a.xptrs[tq]) + static_cast<uintptr_t>(loc) * 4, xn);
+    }
+    a.gbar[je] = Tree<P>::sum(gv) / static_cast<float>(K);
+    a.xc[je] = __builtin_fmaf(a.a, Tree<P>::sum(dv), c);
 }
 
 // ---------------------------------------------------------- launching
@@ -993,17 +1053,26 @@ hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack
     }
 }
 
-template <int P, typename T>
+template <int P, typename T, bool DIRECT>
 hipError_t run_tpipe(const TPipeArgs& a, unsigned blocks, hipStream_t stream) {
     dim3 grid(blocks);
     const int64_t nslot = a.N / 4;
     if ((nslot + 1) * a.K * 16 < (int64_t(1) << 32)) {
-        if (a.gt) hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, true, uint32_t>), grid, dim3(256), 0, stream, a);
-        else hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, false, uint32_t>), grid, dim3(256), 0, stream, a);
+        if (a.gt) hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, true, uint32_t, DIRECT>), grid, dim3(256), 0, stream, a);
+        else hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, false, uint32_t, DIRECT>), grid, dim3(256), 0, stream, a);
     } else {
-        if (a.gt) hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, true, int64_t>), grid, dim3(256), 0, stream, a);
-        else hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, false, int64_t>), grid, dim3(256), 0, stream, a);
+        if (a.gt) hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, true, int64_t, DIRECT>), grid, dim3(256), 0, stream, a);
+        else hipLaunchKernelGGL((tensor_pipeline_kernel<P, T, false, int64_t, DIRECT>), grid, dim3(256), 0, stream, a);
     }
+    return hipGetLastError();
+}
+
+template <int P, typename T>
+hipError_t run_tpipe(const TPipeArgs& a, bool direct, unsigned blocks, hipStream_t stream) {
+    hipError_t e = direct ? run_tpipe<P, T, true>(a, blocks, stream) : run_tpipe<P, T, false>(a, blocks, stream);
+    if (e != hipSuccess || a.N % 4 == 0) return e;
+    if (a.gt) hipLaunchKernelGGL((tensor_pipeline_tail_kernel<P, T, true>), dim3(1), dim3(64), 0, stream, a);
+    else hipLaunchKernelGGL((tensor_pipeline_tail_kernel<P, T, false>), dim3(1), dim3(64), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -1014,9 +1083,13 @@ hipError_t launch_tensor_pipeline(const tc_tensorlist* grads, const tc_tensorlis
                 g->n, grads->K, g->N, g->chunk, eta, rho, eta * rho};
     const unsigned blocks = static_cast<unsigned>(g->nchunks);
     const bool bf16 = grads->elem == 2;
+    // straight between registers and the per-layer tensors when every tensor
+    // boundary before the last, partial slot falls on a slot boundary and
+    // every tensor of both lists is slot-aligned
+    const bool direct = g->slot_bounds && grads->slot_aligned && params->slot_aligned;
     switch (next_pow2(grads->K)) {
 #define TC_CASE(p) \
-    case p: return bf16 ? run_tpipe<p, uint16_t>(a, blocks, stream) : run_tpipe<p, uint32_t>(a, blocks, stream);
+    case p: return bf16 ? run_tpipe<p, uint16_t>(a, direct, blocks, stream) : run_tpipe<p, uint32_t>(a, direct, blocks, stream);
         TC_FOR_P(TC_CASE)
 #undef TC_CASE
         default: return hipErrorInvalidValue;

@@ -181,6 +181,24 @@ def test_misaligned_tensors(orc, K, gdt):
     _run(orc, sizes, K, gdt=gdt, seed=10 + K, misalign=True)
 
 
+@pytest.mark.parametrize("K", [1, 2, 3, 5, 8, 16, 33, 64])
+def test_slot_aligned_groups(orc, K):
+    """Every tensor boundary before the last slot on a slot boundary and
+    every tensor slot-aligned: the kernel moves each chunk straight between
+    registers and the per-layer tensors; the last tensor ends inside a slot,
+    which a launch of its own completes."""
+    sizes = [4096, 8, 0, 12000, 516, 7]
+    _run(orc, sizes, K, seed=70 + K)
+    _run(orc, sizes, K, seed=80 + K, eta=0.125, rho=0.5, integer=True)
+
+
+@pytest.mark.parametrize("gdt", [torch.float32, torch.bfloat16])
+def test_slot_sizes_misaligned_pointers(orc, gdt):
+    """Slot-multiple sizes but tensors one element into their allocations:
+    the tiles and funnel shifts, not the straight path."""
+    _run(orc, [4096, 8, 12000, 516], 8, gdt=gdt, seed=90, misalign=True)
+
+
 @pytest.mark.parametrize("write_g", [True, False])
 def test_without_packed_gradients(orc, write_g):
     _run(orc, [1000, 2051, 17, 40000], 8, seed=3, write_g=write_g)
