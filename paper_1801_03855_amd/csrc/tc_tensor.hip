@@ -670,10 +670,15 @@ struct TPipeArgs {
 
 constexpr int kPipeStage = 512;
 
-// Pieces (slot of one copy) per LDS tile: 256 lanes move TC_PIPE_TILE/256
-// pieces each per phase.
+// Pieces (one slot of one copy) per step of a workgroup: 256 lanes move
+// TILE/256 pieces each.  The straight path (no LDS) holds them in registers;
+// the tiled path stages them in LDS, where smaller tiles leave room for more
+// workgroups per CU (measured on MI355X: 1024 and 512 best respectively).
 #ifndef TC_PIPE_TILE
 #define TC_PIPE_TILE 1024
+#endif
+#ifndef TC_PIPE_TILE_LDS
+#define TC_PIPE_TILE_LDS 512
 #endif
 
 
@@ -689,7 +694,8 @@ template <int P, typename T, bool WG, typename I, bool DIRECT>
 __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
     constexpr int ES = sizeof(T);
     constexpr int SB = 4 * ES;                         // gradient slot bytes
-    constexpr int M = TC_PIPE_TILE / P > 16 ? TC_PIPE_TILE / P : 16;  // slots per tile
+    constexpr int TILE = DIRECT ? TC_PIPE_TILE : TC_PIPE_TILE_LDS;
+    constexpr int M = TILE / P > 16 ? TILE / P : 16;  // slots per tile
     constexpr int R = (M * P) / 256;                                 // pieces per lane and phase
     constexpr int ROWG = (P + 1) * SB, ROWX = (P + 1) * 16;
     __shared__ int32_t s_rel[kPipeStage + 1];
