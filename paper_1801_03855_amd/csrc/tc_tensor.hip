@@ -960,11 +960,12 @@ __global__ __launch_bounds__(64) void tensor_pipeline_tail_kernel(TPipeArgs a) {
 
 // Slots per lane: enough that a wave's single-stream output covers a
 // 128-byte line (P/8 for P >= 16); the reduction takes at least 2, the
-// step 1 (measured).
+// step 1 (measured), and the step at most 4 (8 at P = 64 needed all 256
+// VGPRs, one wave per SIMD).
 // bfloat16 inputs (8-byte slots) take twice the slots to keep as many
 // bytes in flight.
 constexpr int treduce_unroll(int P, int es) { return (P / 8 > 2 ? P / 8 : 2) * (4 / es); }
-constexpr int teasgd_unroll(int P) { return P / 8 > 1 ? P / 8 : 1; }
+constexpr int teasgd_unroll(int P) { return P >= 32 ? 4 : P / 8 > 1 ? P / 8 : 1; }
 
 template <int P, typename T>
 hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hipStream_t s) {

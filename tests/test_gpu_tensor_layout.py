@@ -155,7 +155,7 @@ def test_tensor_integer_inputs_bit_exact(orc, K):
 
 @pytest.mark.parametrize("K,gdt", [(1, torch.float32), (2, torch.float32), (5, torch.float32),
                                    (8, torch.float32), (16, torch.bfloat16), (24, torch.float32),
-                                   (64, torch.bfloat16)])
+                                   (40, torch.float32), (64, torch.bfloat16)])
 def test_easgd_tensor(orc, K, gdt):
     N = 4 * 2049 + 1
     g = tc.Group([N])
