@@ -216,10 +216,12 @@ def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
     print(f"# {layout}: timed {steps} steps in {time.perf_counter() - t0:.3f} s", file=sys.stderr, flush=True)
     per_op_ms = {op: sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(steps)) / steps
                  for i, op in enumerate(ops)}
-    step_ms = sum(ev[s][0].elapsed_time(ev[s][len(ops)]) for s in range(steps)) / steps
+    step_list = sorted(ev[s][0].elapsed_time(ev[s][len(ops)]) for s in range(steps))
+    step_ms = sum(step_list) / steps
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    return {"step_ms": step_ms, "per_op_ms": per_op_ms}
+    return {"step_ms": step_ms, "per_op_ms": per_op_ms, "step_ms_median": step_list[steps // 2],
+            "step_ms_min": step_list[0]}
 
 
 def copy_ceiling(tc, reps: int = 20) -> dict:
@@ -291,6 +293,90 @@ def run_fused(tc, wl, w, sizes, g, steps, warmup):
         out[write_g] = a.elapsed_time(b) / steps
     del grads, X, G, gbar, params, xc
     torch.cuda.empty_cache()
+    return out
+
+
+def _time_launches(fns, reps):
+    """Median and minimum time (ms) of single launches, cycling through the
+    callables in fns (one per input set), from HIP events on the stream."""
+    import torch
+
+    stream = torch.cuda.current_stream()
+    for f in fns:
+        f()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    torch.cuda.synchronize()
+    for r in range(reps):
+        ev[r][0].record(stream)
+        fns[r % len(fns)]()
+        ev[r][1].record(stream)
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) for a, b in ev)
+    return t[reps // 2], t[0]
+
+
+def config_table(tc, wl, reps=20):
+    """Every configured workload's operations on both layouts: median and
+    minimum time of single launches, algorithmic GB/s at the median and its
+    fraction of peak.  The ResNet-50 K = 4 reduction (511 MB per call, about
+    twice the 256 MB last-level cache) is also timed cold, alternating between
+    two input sets; the tiny group is launch-bound, so only its times mean
+    anything there."""
+    import torch
+
+    dev = "cuda"
+    out = {}
+
+    def row(nbytes, fns):
+        med, mn = _time_launches(fns, reps)
+        gbs = nbytes / (med * 1e-3) / 1e9
+        return {"ms_median": round(med, 5), "ms_min": round(mn, 5), "per_s": round(1e3 / med, 1),
+                "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+    for wkey in ("tiny_k2", "resnet50_k4_reduce", "resnet50_k8_easgd", "vgg16_k4_easgd", "many_small_k16_bf16"):
+        w = wl.WORKLOADS[wkey]
+        sizes = w.sizes()
+        g = tc.Group(sizes)
+        N, K = g.numel, w.K
+        s_g = 2 if w.g_dtype == "bf16" else 4
+        print(f"# config {wkey}", file=sys.stderr, flush=True)
+        sets = 2 if wkey == "resnet50_k4_reduce" else 1
+        gsep = [wl.make_gradients(w, N, dev, seed_offset=k) for k in range(sets)]
+        gten = []
+        for gs in gsep:
+            G = torch.empty(tc.tensor_numel(g, K), dtype=gs[0].dtype, device=dev)
+            tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in gs]), G)
+            gten.append(G)
+        avg = torch.empty(N, device=dev)
+        r = {"N": N, "K": K}
+        for op in [o for o in ("reduce_sum", "reduce_avg") if o in w.ops]:
+            kind = op.split("_")[1]
+            nb = op_bytes("reduce", K, N, s_g)
+            r[f"{op} separate"] = row(nb, [lambda gs=gs: tc.reduce(g, gs, avg, kind) for gs in gsep[:1]])
+            r[f"{op} tensor"] = row(nb, [lambda G=G: tc.reduce_tensor(g, K, G, avg, kind) for G in gten[:1]])
+            if sets > 1:
+                r[f"{op} separate, cold"] = row(nb, [lambda gs=gs: tc.reduce(g, gs, avg, kind) for gs in gsep])
+                r[f"{op} tensor, cold"] = row(nb, [lambda G=G: tc.reduce_tensor(g, K, G, avg, kind) for G in gten])
+        if "easgd" in w.ops:
+            xs, xc = wl.make_state(w, N, dev)
+            X = torch.empty(tc.tensor_numel(g, K), device=dev)
+            tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
+            xc2 = xc.clone()
+            nb = op_bytes("easgd", K, N, s_g)
+            r["easgd separate"] = row(nb, [lambda: tc.easgd_step(g, xs, gsep[0], xc, w.eta, w.rho)])
+            r["easgd tensor"] = row(nb, [lambda: tc.easgd_step_tensor(g, K, X, gten[0], xc2, w.eta, w.rho)])
+            if "pack" in w.ops:
+                grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gsep[0]])
+                params = tc.TensorList(g, [[torch.empty(n, device=dev) for n in sizes] for _ in range(K)])
+                r["pipeline (easgd_pipeline_tensor)"] = row(
+                    fused_bytes(K, N, s_g), [lambda: tc.easgd_pipeline_tensor(grads, params, gten[0], avg, X, xc2,
+                                                                              w.eta, w.rho)])
+                del grads, params
+            del xs, xc, X, xc2
+        out[wkey] = r
+        del gsep, gten, avg
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
     return out
 
 
@@ -367,6 +453,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-fused", action="store_true",
                     help="skip timing the one-pass pipeline (easgd_pipeline_tensor)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip timing every configured workload's operations")
     ap.add_argument("--no-next-rows", action="store_true",
                     help="skip timing the schedule and synchronous-SGD operations")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -448,6 +536,10 @@ def main():
                           "traffic": recorded_traffic(args.workload, "tensor").get(
                               "pipeline" if write_g else "pipeline_no_g")}
 
+    configs = None
+    if not args.no_configs:
+        configs = config_table(tc, wl)
+
     extra = None
     if not args.no_next_rows and args.workload == "resnet50_k8_pipeline":
         print("# schedule and synchronous-SGD operations", file=sys.stderr, flush=True)
@@ -466,6 +558,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(step_ms, 5),
+        "ms_per_step_median": round(results[first]["step_ms_median"], 5),
+        "ms_per_step_min": round(results[first]["step_ms_min"], 5),
         "steps_per_s": round(1e3 / step_ms, 2),
         "higher_is_better": True,
         "scaling": "weak",
@@ -478,6 +572,7 @@ def main():
         "layouts": layouts,
         "roofline": roof,
         "fused_pipeline": fused,
+        "configs": configs,
         "next_rows": extra,
         "cpu_baseline": cpu,
     }
