@@ -67,16 +67,20 @@ def op_bytes(op: str, K: int, N: int, s_g: int) -> int:
     raise ValueError(op)
 
 
-# Files whose contents define the kernels measured by the hardware counters.
-KERNEL_SOURCES = ("paper_1801_03855_amd/csrc/tc_elementwise.hip", "paper_1801_03855_amd/csrc/tc_pack.hip",
-                  "paper_1801_03855_amd/csrc/tc_tensor.hip", "paper_1801_03855_amd/csrc/tc_internal.h",
-                  "paper_1801_03855_amd/build.py")
+# Files whose contents define the kernels measured by the hardware counters:
+# every HIP source and header of the library and its build flags.
+def kernel_sources():
+    import glob
+
+    csrc = os.path.join(ROOT, "paper_1801_03855_amd", "csrc")
+    files = sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h")))
+    return [os.path.relpath(f, ROOT) for f in files] + ["include/tc.h", "paper_1801_03855_amd/build.py"]
 
 
 def kernel_source_sha() -> str:
     import hashlib
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in kernel_sources():
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
