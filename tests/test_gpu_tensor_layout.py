@@ -100,6 +100,18 @@ def test_pack_tensor_ragged_and_misaligned(orc, K, dtype):
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=K, misalign=True)
 
 
+@pytest.mark.parametrize("K", [1, 3, 8, 16, 64])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_pack_tensor_slot_aligned(orc, K, dtype):
+    """Slot-multiple tensor lengths before a ragged last tensor, tensors in
+    their own allocations: pack and unpack move each slot straight through
+    registers (the last, partial slot element by element); the same sizes
+    one element into their allocations take the tiles."""
+    sizes = [4096, 8, 0, 12000, 516, 7]
+    _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=20 + K)
+    _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=30 + K, misalign=True)
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_views_and_many_small(orc, dtype):
     _tensor_pack_roundtrip(orc, [1, 2, 3, 5, 8, 13, 4099, 1, 7, 4096, 0, 9001], 4, dtype, seed=5, views=True)
