@@ -529,14 +529,16 @@ def main():
     fused = None
     if not args.no_fused and set(ops) == {"pack", "reduce", "easgd", "unpack"}:
         ft = run_fused(tc, wl, w, sizes, g, args.steps, args.warmup)
-        four_ms = results["tensor"]["step_ms"] if "tensor" in results else None
-        fused = {"entry_point": "easgd_pipeline_tensor", "layout": "tensor"}
+        # against the faster of the measured layouts' four calls
+        four_lay = min(results, key=lambda l: results[l]["step_ms"])
+        four_ms = results[four_lay]["step_ms"]
+        fused = {"entry_point": "easgd_pipeline_tensor", "layout": "tensor", "four_calls_compared": four_lay}
         for write_g, key in ((True, "with_packed_gradients"), (False, "without_packed_gradients")):
             b = fused_bytes(K, N, s_g, write_g)
             gbs = b / (ft[write_g] * 1e-3) / 1e9
             fused[key] = {"ms_per_step": round(ft[write_g], 5), "steps_per_s": round(1e3 / ft[write_g], 2),
                           "algorithmic_bytes": b, "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
-                          "speedup_vs_four_calls": round(four_ms / ft[write_g], 3) if four_ms else None,
+                          "speedup_vs_four_calls": round(four_ms / ft[write_g], 3),
                           "traffic": recorded_traffic(args.workload, "tensor").get(
                               "pipeline" if write_g else "pipeline_no_g")}
 
