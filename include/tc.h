@@ -65,11 +65,11 @@ int32_t tc_version(void);
 /* ------------------------------------------------------------------------
  * Tensor group descriptor.
  *
- * A group is the ordered list of a model's layer tensors (one key per layer,
- * keys in layer order: Sec. 3.2 of the paper) treated as one flat object
- * (the "tensor" of Sec. 6.1).  Tensor t occupies flat positions
- * [offsets[t], offsets[t+1]), offsets[0] = 0, offsets[t+1] = offsets[t] +
- * sizes[t].
+ * A group is the ordered list of a model's layer tensors (one key per weight
+ * tensor, Sec. 3.2 of the paper; the keys visited in tensor order, Sec. 5)
+ * treated as one flat object (the "tensor" of Sec. 6.1).  Tensor t occupies
+ * flat positions [offsets[t], offsets[t+1]), offsets[0] = 0, offsets[t+1] =
+ * offsets[t] + sizes[t].
  *
  * tc_group_create: sizes is a host array of n >= 1 element counts, each
  * >= 0 (zero-size tensors are allowed); it is copied.  Builds the offset

@@ -16,7 +16,8 @@
  * blocking, vectorisation or reordering.
  *
  * Passages followed (sections and equations of the paper):
- *   group offsets   Sec. 3.2: one key per layer tensor, keys in layer order;
+ *   group offsets   Sec. 3.2: one key per weight tensor of the model; Sec. 5:
+ *                   the training loop visits the keys in tensor order;
  *                   Sec. 6.1: a grouping of vectors handled as one object.
  *   pack / unpack   Sec. 3.2: push gathers the tensors of the key list, pull
  *                   copies a value back to every tensor of the list.
