@@ -324,3 +324,57 @@ def test_pipeline_argument_errors():
     assert call() == tc.TC_OK
     assert call(gt=None) == tc.TC_OK
     torch.cuda.synchronize()
+
+
+def test_resnet50_k8_100_iterations_every_path(orc):
+    """ResNet-50 group, K = 8, 100 steps with fixed gradients on three paths
+    at once: easgd_step on separate buffers, easgd_step_tensor, and the
+    one-launch pipeline (packed gradients not written).  With a power-of-two
+    K all three keep the same pairwise order, so the workers and the center
+    stay bit-identical for all 100 steps; a sample of positions is followed
+    by the oracle (the per-step bar on the largest guard magnitude each
+    element reaches)."""
+    w = wl.WORKLOADS["resnet50_k8_easgd"]
+    sizes = w.sizes()
+    g = tc.Group(sizes)
+    N, K = g.numel, w.K
+    gs = wl.make_gradients(w, N, DEV)
+    xs, xc = wl.make_state(w, N, DEV)
+    idx = _sample_index(sizes, N, 91)[::5]
+    ti = torch.from_numpy(idx).to(DEV)
+    h_x = [host_f32(t[ti]) for t in xs]
+    h_g = [host_stored(t[ti]) for t in gs]
+    h_c = host_f32(xc[ti])
+    X = torch.empty(tc.tensor_numel(g, K), device=DEV)
+    G = torch.empty(tc.tensor_numel(g, K), device=DEV)
+    tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
+    tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in gs]), G)
+    Xp, xc_t, xc_p = X.clone(), xc.clone(), xc.clone()
+    grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gs])
+    params = [torch.empty(N, device=DEV) for _ in range(K)]
+    ptl = tc.TensorList(g, [wl.split_views(p, sizes) for p in params])
+    gbar = torch.empty(N, device=DEV)
+    for _ in range(w.iterations):
+        tc.easgd_step(g, xs, gs, xc, w.eta, w.rho)
+        tc.easgd_step_tensor(g, K, X, G, xc_t, w.eta, w.rho)
+        tc.easgd_pipeline_tensor(grads, ptl, None, gbar, Xp, xc_p, w.eta, w.rho)
+    torch.cuda.synchronize()
+    assert torch.equal(xc_t, xc) and torch.equal(xc_p, xc)
+    assert torch.equal(X, Xp)
+    back = [torch.empty(N, device=DEV) for _ in range(K)]
+    tc.unpack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in back]), X)
+    torch.cuda.synchronize()
+    for k in range(K):
+        assert torch.equal(back[k], xs[k]), k
+        assert torch.equal(params[k], xs[k]), k
+    rx = [a.astype(np.float64) for a in h_x]
+    rc = h_c.astype(np.float64)
+    mx, mc = easgd_mags(h_x, h_g, h_c, w.eta, w.rho)
+    for _ in range(w.iterations):
+        orc.easgd_step(rx, h_g, rc, w.eta, w.rho)
+        sx, sc = easgd_mags(rx, h_g, rc, w.eta, w.rho)
+        mx = [np.maximum(a, b) for a, b in zip(mx, sx)]
+        mc = np.maximum(mc, sc)
+    for k in range(K):
+        assert_close(host_f32(xs[k][ti]), rx[k], mx[k], f"x[{k}] after 100 steps")
+    assert_close(host_f32(xc[ti]), rc, mc, "x_c after 100 steps")
