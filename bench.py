@@ -67,23 +67,27 @@ def op_bytes(op: str, K: int, N: int, s_g: int) -> int:
     raise ValueError(op)
 
 
-# Files whose contents define the kernels measured by the hardware counters:
-# every HIP source and header of the library and its build flags (the public
-# header only declares the ABI).
+# What defines the kernels measured by the hardware counters: every HIP source
+# and header of the library, and the compiler flags it is built with (the
+# public header only declares the ABI).
 def kernel_sources():
     import glob
 
     csrc = os.path.join(ROOT, "paper_1801_03855_amd", "csrc")
     files = sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h")))
-    return [os.path.relpath(f, ROOT) for f in files] + ["paper_1801_03855_amd/build.py"]
+    return [os.path.relpath(f, ROOT) for f in files]
 
 
 def kernel_source_sha() -> str:
     import hashlib
+
+    from paper_1801_03855_amd import build as b
+
     h = hashlib.sha256()
     for rel in kernel_sources():
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
+    h.update(" ".join(b.FLAGS).encode())
     return h.hexdigest()
 
 

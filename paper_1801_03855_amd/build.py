@@ -43,11 +43,28 @@ def sources() -> list:
 
 
 def build(output: str = LIBRARY, defines: Sequence[str] = (), verbose: bool = False) -> str:
-    cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines], "-I", INCLUDE, "-I", CSRC,
-           "-o", output + ".tmp", *sources()]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+    """Compiles every source to an object in parallel (the translation units
+    share no device code), then links the shared library."""
+    import tempfile
+    from concurrent.futures import ThreadPoolExecutor
+
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    with tempfile.TemporaryDirectory(prefix="tc_build_") as tmp:
+        jobs = []
+        for src in sources():
+            obj = os.path.join(tmp, os.path.basename(src) + ".o")
+            jobs.append((obj, [HIPCC, *compile_flags, *[f"-D{d}" for d in defines], "-I", INCLUDE, "-I", CSRC,
+                               "-c", src, "-o", obj]))
+
+        def run(cmd):
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            subprocess.run(cmd, check=True)
+
+        with ThreadPoolExecutor(max_workers=min(len(jobs), os.cpu_count() or 1, 8)) as pool:
+            for f in [pool.submit(run, cmd) for _, cmd in jobs]:
+                f.result()
+        run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", output + ".tmp", *[o for o, _ in jobs]])
     os.replace(output + ".tmp", output)
     return output
 

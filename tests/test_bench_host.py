@@ -45,7 +45,14 @@ def test_counter_summaries_are_tied_to_every_kernel_source():
     csrc = os.path.join(ROOT, "paper_1801_03855_amd", "csrc")
     for f in glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h")):
         assert os.path.relpath(f, ROOT) in listed, f
-    assert "paper_1801_03855_amd/build.py" in listed
+
+
+def test_counter_summaries_are_tied_to_the_compiler_flags(monkeypatch):
+    from paper_1801_03855_amd import build as b
+
+    sha = bench.kernel_source_sha()
+    monkeypatch.setattr(b, "FLAGS", b.FLAGS + ["-DSOMETHING_ELSE"])
+    assert bench.kernel_source_sha() != sha
 
 
 def test_recorded_traffic_matches_algorithmic_bytes_when_current():
