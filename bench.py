@@ -471,7 +471,7 @@ def main():
                          "reference for scaling hardware byte counters, and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: this build models the K workers as K resident copies "
+        print(f"bench.py measures one GPU: the library models the K workers as K resident copies "
               f"in one GPU's memory and has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
