@@ -185,8 +185,8 @@ int32_t easgd_step_ex(const tc_group* g, int32_t K, float* const* x,
                       float eta, float rho, void* stream);
 
 /* ------------------------------------------------------------------------
- * Tensor layout.  The paper's "tensor" (Sec. 6.1) is a grouping of vectors,
- * one from each worker, operated on as one unit.  In this layout the K
+ * Tensor layout.  The paper's "tensor" (Sec. 6.1) collects one vector per
+ * worker and treats the set as a single unit.  In this layout the K
  * copies of a group live in ONE buffer, interleaved in slots of four
  * consecutive elements: element e of copy i is at index
  *

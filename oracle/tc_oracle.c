@@ -18,7 +18,7 @@
  * Passages followed (sections and equations of the paper):
  *   group offsets   Sec. 3.2: one key per weight tensor of the model; Sec. 5:
  *                   the training loop visits the keys in tensor order;
- *                   Sec. 6.1: a grouping of vectors handled as one object.
+ *                   Sec. 6.1: a set of vectors treated as a single unit.
  *   pack / unpack   Sec. 3.2: push gathers the tensors of the key list, pull
  *                   copies a value back to every tensor of the list.
  *   reduce          Sec. 2.2: workers wait for the global average of the
@@ -39,8 +39,8 @@
  *                   1/mini_batch_size.
  *   broadcast       Sec. 3.2: pull copies one value to every tensor of the
  *                   list.
- *   tensor layout   Sec. 6.1: a "tensor" is a grouping of vectors, one from
- *                   each worker, handled as one unit.  Here the K copies
+ *   tensor layout   Sec. 6.1: a "tensor" collects one vector per worker and
+ *                   treats the set as a single unit.  Here the K copies
  *                   are held in one buffer, interleaved in slots of four
  *                   consecutive elements (an index map of this library's
  *                   design, written out plainly below).
