@@ -158,11 +158,43 @@ def cpu_baseline(wkey: str, ops, sample_elems: int = 30_000_000, min_seconds: fl
         reps += 1
     secs = sum(t[o] for o in ops)
     nbytes = reps * sum(op_bytes(o, w.K, n, s_g) for o in ops)
-    return {"value": round(nbytes / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{reps} passes of {'+'.join(ops)} over the first {len(sub)} tensors of the group "
-                      f"({n} elements, K={w.K}); binary64 C oracle, 1 thread",
-            "seconds": round(secs, 3),
-            "steps_per_s": round(reps * n / (secs * sum(sizes)), 4)}
+    out = {"value": round(nbytes / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+           "sample": f"{reps} passes of {'+'.join(ops)} over the first {len(sub)} tensors of the group "
+                     f"({n} elements, K={w.K}); binary64 C oracle, 1 thread",
+           "seconds": round(secs, 3),
+           "steps_per_s": round(reps * n / (secs * sum(sizes)), 4)}
+
+    # the same oracle functions on every host core: each thread takes a
+    # contiguous block of whole tensors through the four operations (the
+    # operations are elementwise, so the blocks never share an element)
+    from concurrent.futures import ThreadPoolExecutor
+
+    threads = max(1, min(16, os.cpu_count() or 1))
+    offs = np.cumsum([0] + sub)
+    bounds = [int(np.searchsorted(offs, n * j / threads)) for j in range(threads)] + [len(sub)]
+    blocks = [(a, b) for a, b in zip(bounds[:-1], bounds[1:]) if b > a]
+
+    def block_pass(a, b):
+        lo, hi = int(offs[a]), int(offs[b])
+        packed = [orc.pack(p[a:b]) for p in g_parts]
+        orc.reduce(packed, oracle.AVG)
+        xb = [x[lo:hi] for x in x64]
+        orc.easgd_step(xb, packed, c64[lo:hi], w.eta, w.rho)
+        for x in xb:
+            orc.unpack(x.astype(np.float32), sub[a:b])
+
+    with ThreadPoolExecutor(max_workers=len(blocks)) as pool:
+        preps, t0 = 0, time.perf_counter()
+        while preps < max_reps and (preps == 0 or time.perf_counter() - t0 < min_seconds / 2):
+            list(pool.map(lambda ab: block_pass(*ab), blocks))
+            preps += 1
+        psecs = time.perf_counter() - t0
+    out["parallel"] = {"value": round(preps * sum(op_bytes(o, w.K, n, s_g) for o in ops) / psecs / 1e9, 3),
+                       "unit": "GB/s", "cores": len(blocks), "kind": "oracle",
+                       "sample": f"{preps} passes of the same sample, {len(blocks)} threads, each taking a "
+                                 f"block of whole tensors through {'+'.join(ops)}",
+                       "seconds": round(psecs, 3)}
+    return out
 
 
 def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
