@@ -536,35 +536,66 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
         constexpr int R = (M * P) / 256;
         if (!UNPACK) {
             // copies -> tile: lanes walk consecutive slots of one copy
-            u4 v[R];
-            bool ok[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int q = threadIdx.x + r * 256;
-                const int kk = q / M, jl = q % M;
-                ok[r] = kk < K && jl < mt;
-                if (!ok[r]) continue;
-                const int js = t0 + jl, jr = 4 * js;
+            auto slot_piece = [&](int kk, int js) -> u4 {  // one slot of copy kk
+                const int jr = 4 * js;
                 int s = find(jr);
-                if (jr + 4 <= rel(s + 1)) {
-                    v[r] = load_bytes<SB>(base(kk, s) + static_cast<uintptr_t>(jr) * ES);
-                } else {  // the slot spans tensors
-                    T e4[4];
+                if (jr + 4 <= rel(s + 1)) return load_bytes<SB>(base(kk, s) + static_cast<uintptr_t>(jr) * ES);
+                T e4[4];  // the slot spans tensors
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        while (jr + e >= rel(s + 1)) ++s;
-                        e4[e] = gld<T>(base(kk, s) + static_cast<uintptr_t>(jr + e) * ES);
-                    }
-                    v[r] = u4{0u, 0u, 0u, 0u};
-                    __builtin_memcpy(&v[r], e4, SB);
+                for (int e = 0; e < 4; ++e) {
+                    while (jr + e >= rel(s + 1)) ++s;
+                    e4[e] = gld<T>(base(kk, s) + static_cast<uintptr_t>(jr + e) * ES);
                 }
-            }
+                u4 v = u4{0u, 0u, 0u, 0u};
+                __builtin_memcpy(&v, e4, SB);
+                return v;
+            };
+            if constexpr (SB == 16) {
+                u4 v[R];
+                bool ok[R];
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                if (!ok[r]) continue;
-                const int q = threadIdx.x + r * 256;
-                if constexpr (SB == 16) *reinterpret_cast<u4*>(tile(q % M, q / M)) = v[r];
-                else *reinterpret_cast<u2*>(tile(q % M, q / M)) = u2{v[r].x, v[r].y};
+                for (int r = 0; r < R; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    const int kk = q / M, jl = q % M;
+                    ok[r] = kk < K && jl < mt;
+                    if (ok[r]) v[r] = slot_piece(kk, t0 + jl);
+                }
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    if (ok[r]) *reinterpret_cast<u4*>(tile(q % M, q / M)) = v[r];
+                }
+            } else {
+                // 8-byte slots: a lane takes two consecutive slots of one copy,
+                // 16 source bytes read as one (funnel-shifted) granule pair
+                // when both lie in one tensor
+                constexpr int R2 = R / 2, MH = M / 2;
+                u4 v[R2];
+                bool ok0[R2], ok1[R2];
+#pragma unroll
+                for (int r = 0; r < R2; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    const int kk = q / MH, jl = 2 * (q % MH);
+                    ok0[r] = kk < K && jl < mt;
+                    ok1[r] = kk < K && jl + 1 < mt;
+                    if (!ok0[r]) continue;
+                    const int jr = 4 * (t0 + jl);
+                    const int s = find(jr);
+                    if (ok1[r] && jr + 8 <= rel(s + 1)) {
+                        v[r] = load_bytes<16>(base(kk, s) + static_cast<uintptr_t>(jr) * ES);
+                    } else {
+                        const u4 a0 = slot_piece(kk, t0 + jl);
+                        const u4 a1 = ok1[r] ? slot_piece(kk, t0 + jl + 1) : u4{0u, 0u, 0u, 0u};
+                        v[r] = u4{a0.x, a0.y, a1.x, a1.y};
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < R2; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    const int kk = q / MH, jl = 2 * (q % MH);
+                    if (ok0[r]) *reinterpret_cast<u2*>(tile(jl, kk)) = u2{v[r].x, v[r].y};
+                    if (ok1[r]) *reinterpret_cast<u2*>(tile(jl + 1, kk)) = u2{v[r].z, v[r].w};
+                }
             }
             __syncthreads();
             // tile -> tensor, in tensor order
@@ -842,35 +873,65 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
         const int mt = nsl - t0 < M ? nsl - t0 : M;
         // gather: gradients into the tile; workers and center in registers
         {
-            u4 v[R];
-            bool ok[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int q = threadIdx.x + r * 256;
-                const int kk = q / M, jl = q % M;
-                ok[r] = kk < K && jl < mt;
-                if (!ok[r]) continue;
-                const int jr = 4 * (t0 + jl);
+            auto slot_piece = [&](int kk, int js) -> u4 {  // one slot of copy kk
+                const int jr = 4 * js;
                 int s = find(jr);
-                if (jr + 4 <= rel(s + 1)) {
-                    v[r] = load_bytes<SB>(gbase(kk, s) + static_cast<uintptr_t>(jr) * ES);
-                } else {  // the slot spans tensors
-                    T e4[4];
+                if (jr + 4 <= rel(s + 1)) return load_bytes<SB>(gbase(kk, s) + static_cast<uintptr_t>(jr) * ES);
+                T e4[4];  // the slot spans tensors
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        while (jr + e >= rel(s + 1)) ++s;
-                        e4[e] = gld<T>(gbase(kk, s) + static_cast<uintptr_t>(jr + e) * ES);
-                    }
-                    v[r] = u4{0u, 0u, 0u, 0u};
-                    __builtin_memcpy(&v[r], e4, SB);
+                for (int e = 0; e < 4; ++e) {
+                    while (jr + e >= rel(s + 1)) ++s;
+                    e4[e] = gld<T>(gbase(kk, s) + static_cast<uintptr_t>(jr + e) * ES);
                 }
-            }
+                u4 v = u4{0u, 0u, 0u, 0u};
+                __builtin_memcpy(&v, e4, SB);
+                return v;
+            };
+            if constexpr (SB == 16) {
+                u4 v[R];
+                bool ok[R];
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                if (!ok[r]) continue;
-                const int q = threadIdx.x + r * 256;
-                if constexpr (SB == 16) *reinterpret_cast<u4*>(gtile(q % M, q / M)) = v[r];
-                else *reinterpret_cast<u2*>(gtile(q % M, q / M)) = u2{v[r].x, v[r].y};
+                for (int r = 0; r < R; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    const int kk = q / M, jl = q % M;
+                    ok[r] = kk < K && jl < mt;
+                    if (ok[r]) v[r] = slot_piece(kk, t0 + jl);
+                }
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    if (ok[r]) *reinterpret_cast<u4*>(gtile(q % M, q / M)) = v[r];
+                }
+            } else {
+                // 8-byte slots: two consecutive slots of one copy per lane, as
+                // in tc_pack_tensor
+                constexpr int R2 = R / 2, MH = M / 2;
+                u4 v[R2];
+                bool ok0[R2], ok1[R2];
+#pragma unroll
+                for (int r = 0; r < R2; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    const int kk = q / MH, jl = 2 * (q % MH);
+                    ok0[r] = kk < K && jl < mt;
+                    ok1[r] = kk < K && jl + 1 < mt;
+                    if (!ok0[r]) continue;
+                    const int jr = 4 * (t0 + jl);
+                    const int s = find(jr);
+                    if (ok1[r] && jr + 8 <= rel(s + 1)) {
+                        v[r] = load_bytes<16>(gbase(kk, s) + static_cast<uintptr_t>(jr) * ES);
+                    } else {
+                        const u4 a0 = slot_piece(kk, t0 + jl);
+                        const u4 a1 = ok1[r] ? slot_piece(kk, t0 + jl + 1) : u4{0u, 0u, 0u, 0u};
+                        v[r] = u4{a0.x, a0.y, a1.x, a1.y};
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < R2; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    const int kk = q / MH, jl = 2 * (q % MH);
+                    if (ok0[r]) *reinterpret_cast<u2*>(gtile(jl, kk)) = u2{v[r].x, v[r].y};
+                    if (ok1[r]) *reinterpret_cast<u2*>(gtile(jl + 1, kk)) = u2{v[r].z, v[r].w};
+                }
             }
         }
         f4 xv[R], cv[R];
