@@ -176,6 +176,8 @@ class TensorList:
 
     def __init__(self, group: Group, tensors: Sequence[Sequence[torch.Tensor]]):
         K = len(tensors)
+        if K < 1:
+            raise ValueError("a tensor list needs at least one copy")
         dt = None
         ptrs = []
         for k, copy in enumerate(tensors):
