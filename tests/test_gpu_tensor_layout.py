@@ -165,7 +165,8 @@ def test_tensor_integer_inputs_bit_exact(orc, K):
 
 # ------------------------------------------------------------------- easgd
 
-@pytest.mark.parametrize("K,gdt", [(1, torch.float32), (2, torch.float32), (5, torch.float32),
+@pytest.mark.parametrize("K,gdt", [(1, torch.float32), (2, torch.float32), (3, torch.bfloat16), (4, torch.float32),
+                                   (5, torch.float32),
                                    (8, torch.float32), (16, torch.bfloat16), (24, torch.float32),
                                    (40, torch.float32), (64, torch.bfloat16)])
 def test_easgd_tensor(orc, K, gdt):
