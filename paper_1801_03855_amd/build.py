@@ -72,9 +72,15 @@ def build(output: str = LIBRARY, defines: Sequence[str] = (), verbose: bool = Fa
 if __name__ == "__main__":
     out = LIBRARY
     defs = []
-    for arg in sys.argv[1:]:
+    args = sys.argv[1:]
+    while args:
+        arg = args.pop(0)
         if arg.startswith("-D"):
-            defs.append(arg[2:])
+            defs.append(arg[2:] or args.pop(0))
         elif arg.startswith("-o"):
-            out = arg[2:]
-    print(build(out, defs, verbose=True))
+            out = arg[2:] or args.pop(0)
+        else:
+            sys.exit(f"usage: python -m paper_1801_03855_amd.build [-D NAME=VALUE ...] [-o OUTPUT.so] (got {arg!r})")
+    if not out:
+        sys.exit("empty output path")
+    print(build(os.path.abspath(out), defs, verbose=True))
