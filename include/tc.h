@@ -20,6 +20,12 @@
  *   Every data operation is enqueued asynchronously on it, and nothing waits
  *   for it to finish; faults during execution surface at the caller's next
  *   synchronisation.
+ * - Data operations allocate nothing, copy nothing between host and device
+ *   and never synchronise: they only enqueue kernels, whose arguments carry
+ *   the pointers of the call.  A sequence of them can be captured in a HIP
+ *   graph and replayed; the descriptors it names (and their device tables)
+ *   must then outlive the graph.  Only tc_group_create/_destroy and
+ *   tc_tensorlist_create/_destroy allocate, copy and free.
  * - Return value of the data operations: TC_OK, or a negative tc_status.
  *   On error nothing has been enqueued, except TC_EHIP from a failed launch;
  *   tc_last_error() then describes the error (thread-local, valid until the

@@ -378,3 +378,102 @@ def test_resnet50_k8_100_iterations_every_path(orc):
     for k in range(K):
         assert_close(host_f32(xs[k][ti]), rx[k], mx[k], f"x[{k}] after 100 steps")
     assert_close(host_f32(xc[ti]), rc, mc, "x_c after 100 steps")
+
+
+def test_steps_replay_from_a_hip_graph():
+    """Every data entry point only launches kernels (no allocation, no
+    synchronisation, no memset), so a step can be captured in a HIP graph.
+    The four calls and the one-launch pipeline are captured once and
+    replayed five times, with eager work and synchronisations between the
+    replays; after every replay the state equals the same number of eager
+    steps, bit for bit."""
+    w = wl.WORKLOADS["tiny_k2"]
+    sizes = w.sizes()
+    g = tc.Group(sizes)
+    N, K = g.numel, w.K
+    gflat = wl.make_gradients(w, N, DEV)
+    xs, xc = wl.make_state(w, N, DEV)
+    grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gflat])
+
+    def make():
+        X = torch.empty(tc.tensor_numel(g, K), device=DEV)
+        tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
+        G = torch.empty(tc.tensor_numel(g, K), device=DEV)
+        params = [torch.empty(N, device=DEV) for _ in range(K)]
+        return dict(X=X, G=G, c=xc.clone(), gbar=torch.empty(N, device=DEV), params=params,
+                    ptl=tc.TensorList(g, [wl.split_views(p, sizes) for p in params]))
+
+    def four(st, s):
+        tc.pack_tensor(grads, st["G"], s)
+        tc.reduce_tensor(g, K, st["G"], st["gbar"], "avg", s)
+        tc.easgd_step_tensor(g, K, st["X"], st["G"], st["c"], w.eta, w.rho, s)
+        tc.unpack_tensor(st["ptl"], st["X"], s)
+
+    def one(st, s):
+        tc.easgd_pipeline_tensor(grads, st["ptl"], st["G"], st["gbar"], st["X"], st["c"], w.eta, w.rho, s)
+
+    for step in (four, one):
+        eager, graphed = make(), make()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            step(graphed, side)  # recorded, not run
+        torch.cuda.synchronize()
+        for rep in range(5):
+            graph.replay()
+            step(eager, torch.cuda.current_stream())
+            torch.cuda.synchronize()
+            scratch = torch.randn(1 << 16, device=DEV).sum()  # unrelated eager work between replays
+            for key in ("X", "G", "c", "gbar"):
+                assert torch.equal(graphed[key], eager[key]), (step.__name__, rep, key)
+            for k in range(K):
+                assert torch.equal(graphed["params"][k], eager["params"][k]), (step.__name__, rep, k)
+            del scratch
+        del graph
+
+
+def test_separate_buffer_step_replays_from_a_hip_graph():
+    """The separate-buffer step (pack, AVG, fused step, unpack; the pointer
+    arrays travel as launch arguments) captured once and replayed five times
+    equals five eager steps bit for bit after every replay."""
+    w = wl.WORKLOADS["tiny_k2"]
+    sizes = w.sizes()
+    g = tc.Group(sizes)
+    N, K = g.numel, w.K
+    gflat = wl.make_gradients(w, N, DEV)
+    xs, xc = wl.make_state(w, N, DEV)
+    grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gflat])
+
+    def make():
+        st = dict(x=[t.clone() for t in xs], c=xc.clone(), gbar=torch.empty(N, device=DEV),
+                  g=[torch.empty(N, device=DEV) for _ in range(K)], p=[torch.empty(N, device=DEV) for _ in range(K)])
+        st["ptl"] = tc.TensorList(g, [wl.split_views(p, sizes) for p in st["p"]])
+        return st
+
+    def step(st, s):
+        tc.pack(grads, st["g"], s)
+        tc.reduce(g, st["g"], st["gbar"], "avg", s)
+        tc.easgd_step(g, st["x"], st["g"], st["c"], w.eta, w.rho, s)
+        tc.unpack(st["ptl"], st["x"], s)
+
+    eager, graphed = make(), make()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        step(graphed, side)
+    torch.cuda.synchronize()
+    for rep in range(5):
+        graph.replay()
+        step(eager, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        scratch = torch.randn(1 << 16, device=DEV).sum()
+        assert torch.equal(graphed["c"], eager["c"]) and torch.equal(graphed["gbar"], eager["gbar"]), rep
+        for k in range(K):
+            for key in ("x", "g", "p"):
+                assert torch.equal(graphed[key][k], eager[key][k]), (rep, key, k)
+        del scratch
+    del graph
