@@ -35,6 +35,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -78,15 +79,26 @@ def kernel_sources():
     return [os.path.relpath(f, ROOT) for f in files]
 
 
+# C/C++ comments, and string or character literals kept as they are
+_COMMENT = re.compile(r'("(?:\\.|[^"\\\n])*"|\'(?:\\.|[^\'\\\n])*\')|//[^\n]*|/\*.*?\*/', re.S)
+
+
+def strip_comments(text: str) -> str:
+    return _COMMENT.sub(lambda m: m.group(1) or "", text)
+
+
 def kernel_source_sha() -> str:
+    """Hash of what the kernels are compiled from: every source with its
+    comments removed, and the compiler flags.  Editing a comment leaves it
+    unchanged; any change to code or flags changes it."""
     import hashlib
 
     from paper_1801_03855_amd import build as b
 
     h = hashlib.sha256()
     for rel in kernel_sources():
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(strip_comments(f.read()).encode())
     h.update(" ".join(b.FLAGS).encode())
     return h.hexdigest()
 

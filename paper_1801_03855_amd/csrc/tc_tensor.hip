@@ -138,6 +138,18 @@ struct Tree<1> {
     static __device__ __forceinline__ float sum(float* v) { return v[0]; }
 };
 
+// s / K, correctly rounded.  When K = P (a power of two) 1/K is exact, so
+// the product with it rounds the same exact quotient: one multiply instead
+// of the division sequence.  K is uniform, so the branch is too.
+template <int P>
+__device__ __forceinline__ float div_k(float s, int K) {
+    return K == P ? s * (1.0f / P) : s / static_cast<float>(K);
+}
+template <int P>
+__device__ __forceinline__ f4 div_k(f4 s, int K) {
+    return K == P ? s * f4(1.0f / P) : s / f4(static_cast<float>(K));
+}
+
 // First slot of this lane: a workgroup covers 4*U*(64/P) consecutive
 // slots, each wave U*(64/P) of them, so the single-stream outputs (the
 // reduction, the center) leave every wave as >= 128 contiguous bytes.
@@ -158,33 +170,54 @@ struct TReduceArgs {
     int K, op;
 };
 
-// P: lanes per slot (K rounded up to a power of two).
-template <int P, typename T, int U, typename I>
+// Two consecutive bfloat16 slots (copies s and s + 1 of one slot, s even,
+// 16-byte aligned) summed component-wise: the first level of the pairwise
+// tree, taken inside the lane.
+template <typename I>
+__device__ __forceinline__ f4 load_pair_sum(const uint16_t* p, I s) {
+    const u4 w = __builtin_nontemporal_load(reinterpret_cast<const u4*>(reinterpret_cast<const char*>(p) + s * I(8)));
+    const f4 lo{__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u), __uint_as_float(w.y << 16),
+                __uint_as_float(w.y & 0xffff0000u)};
+    const f4 hi{__uint_as_float(w.z << 16), __uint_as_float(w.z & 0xffff0000u), __uint_as_float(w.w << 16),
+                __uint_as_float(w.w & 0xffff0000u)};
+    return lo + hi;
+}
+
+// P: K rounded up to a power of two.  One lane per copy (L = P lanes per
+// slot), or, for bfloat16 with K even (PAIR), one lane per two copies
+// (L = P / 2): each lane loads 16 bytes and adds its pair first, which is
+// the tree's first level, so the butterfly over the L lanes finishes the
+// same sum in one fewer step with half the lanes.
+template <int P, typename T, int U, typename I, bool PAIR>
 __global__ __launch_bounds__(256) void tensor_reduce_kernel(TReduceArgs<T> a) {
-    constexpr int SPW = 64 / P;  // slots per wave and unroll step
+    constexpr int L = PAIR ? P / 2 : P;
+    constexpr int SPW = 64 / L;  // slots per wave and unroll step
     const int K = a.K;
-    const int i = threadIdx.x % P;
-    const I j0 = first_slot<P, U, I>();
+    const int i = threadIdx.x % L;
+    const I j0 = first_slot<L, U, I>();
     const I nslot = static_cast<I>(a.nslot);
     f4 v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const I j = j0 + I(u) * SPW;
-        v[u] = (j < nslot && i < K) ? load_slot(a.in, j * I(K) + I(i)) : f4(0.0f);
+        if constexpr (PAIR)
+            v[u] = (j < nslot && 2 * i < K) ? load_pair_sum(a.in, j * I(K) + I(2 * i)) : f4(0.0f);
+        else
+            v[u] = (j < nslot && i < K) ? load_slot(a.in, j * I(K) + I(i)) : f4(0.0f);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const I j = j0 + I(u) * SPW;
-        if constexpr (P >= 4) {
+        if constexpr (L >= 4) {
             // lanes 0-3 of the group hold one component each
-            float s = split_group_sum<P>(v[u], threadIdx.x);
-            if (a.op == TC_AVG) s = s / static_cast<float>(K);  // correctly rounded
+            float s = split_group_sum<L>(v[u], threadIdx.x);
+            if (a.op == TC_AVG) s = div_k<P>(s, K);
             if (j < nslot && i < 4)
                 __builtin_nontemporal_store(s, reinterpret_cast<float*>(reinterpret_cast<char*>(a.out) + j * I(16)) +
                                                    comp_of_lane(i));
         } else {
-            f4 s = group_sum4<P>(v[u]);
-            if (a.op == TC_AVG) s = s / f4(static_cast<float>(K));  // correctly rounded
+            f4 s = group_sum4<L>(v[u]);
+            if (a.op == TC_AVG) s = div_k<P>(s, K);
             if (j < nslot && i == 0) store_slot(a.out, j, s);
         }
     }
@@ -196,7 +229,7 @@ __global__ __launch_bounds__(256) void tensor_reduce_kernel(TReduceArgs<T> a) {
             for (int q = 0; q < P; ++q)
                 t[q] = q < K ? load_elem(a.in, (a.nslot * K + q) * 4 + (e & 3)) : 0.0f;
             float s = Tree<P>::sum(t);
-            if (a.op == TC_AVG) s = s / static_cast<float>(K);
+            if (a.op == TC_AVG) s = div_k<P>(s, K);
             a.out[e] = s;
         }
     }
@@ -805,7 +838,6 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
     auto xtile = [&](int jl, int kk) -> unsigned char* { return s_tile + jl * ROWX + kk * 16; };
     const int64_t slot0 = cstart / 4;
     const f4 rho = f4(a.rho), neg_eta = f4(-a.eta), alpha = f4(a.a);
-    const float kf = static_cast<float>(K);
     // The step on one piece (slot J of worker i): the packed gradient out,
     // the AVG and the center from the split butterflies, the new worker out
     // and returned.  Every lane calls it (the butterflies need all lanes).
@@ -817,7 +849,7 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
         const f4 xn = fma4(neg_eta, fma4(rho, d, g), x);
         if constexpr (P >= 4) {
             // lanes 0-3 of the slot's group hold one component each
-            const float gs = split_group_sum<P>(g, threadIdx.x) / kf;  // correctly rounded
+            const float gs = div_k<P>(split_group_sum<P>(g, threadIdx.x), K);
             const float ds = split_group_sum<P>(d, threadIdx.x);
             const int cp = comp_of_lane(i);
             if (slot && i < 4) {
@@ -825,7 +857,7 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
                 __builtin_nontemporal_store(__builtin_fmaf(a.a, ds, comp(c, cp)), a.xc + (J * I(4) + I(cp)));
             }
         } else {
-            const f4 gs = group_sum4<P>(g) / f4(kf);
+            const f4 gs = div_k<P>(group_sum4<P>(g), K);
             const f4 cn = fma4(alpha, group_sum4<P>(d), c);
             if (slot && i == 0) {
                 store_slot(a.gbar, J, gs);
@@ -1043,7 +1075,7 @@ __global__ __launch_bounds__(64) void tensor_pipeline_tail_kernel(TPipeArgs a) {
         a.x[idx] = xn;
         gst<float>(reinterpret_cast<uintptr_t>(a.xptrs[tq]) + static_cast<uintptr_t>(loc) * 4, xn);
     }
-    a.gbar[je] = Tree<P>::sum(gv) / static_cast<float>(K);
+    a.gbar[je] = div_k<P>(Tree<P>::sum(gv), K);
     a.xc[je] = __builtin_fmaf(a.a, Tree<P>::sum(dv), c);
 }
 
@@ -1053,27 +1085,49 @@ __global__ __launch_bounds__(64) void tensor_pipeline_tail_kernel(TPipeArgs a) {
 // 128-byte line (P/8 for P >= 16); the reduction takes at least 2, the
 // step 1 (measured), and the step at most 4 (8 at P = 64 needed all 256
 // VGPRs, one wave per SIMD).
-// bfloat16 inputs (8-byte slots) take four times the slots, at most 16
-// (measured at K = 16: 4.6 TB/s with twice, 4.9 with four times, 3.9 with
-// eight times the binary32 count).
+// bfloat16 inputs read one copy per lane (odd K; 8-byte slots) take four
+// times the slots, at most 16 (measured at K = 16: 4.6 TB/s with twice, 4.9
+// with four times, 3.9 with eight times the binary32 count).
 constexpr int treduce_unroll(int P, int es) {
     const int u = P / 8 > 2 ? P / 8 : 2;
     return es == 2 ? (4 * u < 16 ? 4 * u : 16) : u;
 }
+// bfloat16 pairs (even K; 16 bytes per lane, L = P / 2 lanes per slot):
+// the binary32 count for L lanes, times TC_TREDUCE_PAIR_SCALE, at most 16
+// (measured at K = 16: 6.27-6.34 TB/s once, 6.35-6.40 twice, 6.21-6.26
+// four times).
+#ifndef TC_TREDUCE_PAIR_SCALE
+#define TC_TREDUCE_PAIR_SCALE 2
+#endif
+#ifndef TC_TREDUCE_PAIR
+#define TC_TREDUCE_PAIR 1
+#endif
+constexpr int treduce_pair_unroll(int L) {
+    const int u = TC_TREDUCE_PAIR_SCALE * (L / 8 > 2 ? L / 8 : 2);
+    return u < 16 ? u : 16;
+}
 constexpr int teasgd_unroll(int P) { return P >= 32 ? 4 : P / 8 > 1 ? P / 8 : 1; }
 
-template <int P, typename T>
-hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hipStream_t s) {
-    constexpr int U = treduce_unroll(P, sizeof(T));
-    constexpr int SPB = 256 / P;
+template <int P, typename T, bool PAIR>
+hipError_t run_treduce_as(int K, const void* in, float* out, int op, int64_t n, hipStream_t s) {
+    constexpr int L = PAIR ? P / 2 : P;
+    constexpr int U = PAIR ? treduce_pair_unroll(L) : treduce_unroll(P, sizeof(T));
+    constexpr int SPB = 256 / L;
     TReduceArgs<T> a{static_cast<const T*>(in), out, n / 4, n, K, op};
     const int64_t blocks = (a.nslot + SPB * U - 1) / (SPB * U);
     dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
     if ((a.nslot + 1) * K * 16 < (int64_t(1) << 32))
-        hipLaunchKernelGGL((tensor_reduce_kernel<P, T, U, uint32_t>), grid, dim3(256), 0, s, a);
+        hipLaunchKernelGGL((tensor_reduce_kernel<P, T, U, uint32_t, PAIR>), grid, dim3(256), 0, s, a);
     else
-        hipLaunchKernelGGL((tensor_reduce_kernel<P, T, U, int64_t>), grid, dim3(256), 0, s, a);
+        hipLaunchKernelGGL((tensor_reduce_kernel<P, T, U, int64_t, PAIR>), grid, dim3(256), 0, s, a);
     return hipGetLastError();
+}
+
+template <int P, typename T>
+hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hipStream_t s) {
+    if constexpr (sizeof(T) == 2 && P >= 2)
+        if (TC_TREDUCE_PAIR && K % 2 == 0) return run_treduce_as<P, T, true>(K, in, out, op, n, s);
+    return run_treduce_as<P, T, false>(K, in, out, op, n, s);
 }
 
 template <int P, typename T>

@@ -71,3 +71,19 @@ def test_recorded_traffic_matches_algorithmic_bytes_when_current():
                 alg = (bench.fused_bytes(w.K, n, s_g, op == "pipeline") if op.startswith("pipeline")
                        else bench.op_bytes(op, w.K, n, s_g))
                 assert abs(traffic / alg - 1) < 5e-3, (wname, lay, op, traffic, alg)
+
+
+def test_source_hash_ignores_comments_only(tmp_path, monkeypatch):
+    """The hash that ties counter summaries to the kernels ignores comments
+    (they do not change the compiled code) but sees any change to code,
+    including inside string literals that contain comment markers."""
+    src = tmp_path / "k.hip"
+    monkeypatch.setattr(bench, "kernel_sources", lambda: [str(src)])
+    src.write_text('int f() { return 1; } // one\n/* two */ const char* s = "a // b";\n')
+    h0 = bench.kernel_source_sha()
+    src.write_text('int f() { return 1; } // changed\n/* also\n changed */ const char* s = "a // b";\n')
+    assert bench.kernel_source_sha() == h0
+    src.write_text('int f() { return 2; } // one\n/* two */ const char* s = "a // b";\n')
+    assert bench.kernel_source_sha() != h0
+    src.write_text('int f() { return 1; } // one\n/* two */ const char* s = "a // c";\n')
+    assert bench.kernel_source_sha() != h0

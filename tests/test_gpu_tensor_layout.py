@@ -137,6 +137,30 @@ def test_reduce_tensor(orc, K, dtype):
         assert_close(host_f32(out), orc.reduce(copies, code), reduce_mag(copies, op == "avg"), f"K={K} {op}")
 
 
+@pytest.mark.parametrize("K", [2, 3, 6, 16, 33, 64])
+def test_reduce_tensor_bf16_pairs(orc, K):
+    """bfloat16 copies with K even are read two per lane, which adds each
+    pair before the butterfly (the pairwise tree's first level).  Both
+    layouts add in that tree, so the tensor layout's SUM and AVG equal the
+    separate-buffer reduction bit for bit on general inputs; integers that
+    bfloat16 holds exactly (|v| <= 256) give the oracle's sums exactly."""
+    N = 4 * 2053 + 1
+    g = tc.Group([N])
+    for name, copies in (("general", _make_copies(N, K, torch.bfloat16, seed=40 + K)),
+                         ("integer", [c.to(torch.bfloat16) for c in
+                                      wl.integer_values(N, K, 256, seed=50 + K, device=DEV)])):
+        host = _to_tensor_layout(orc, copies, fill=0)
+        T = _device_tensor(host, torch.bfloat16)
+        for op, code in (("sum", oracle.SUM), ("avg", oracle.AVG)):
+            got, sep = torch.empty(N, device=DEV), torch.empty(N, device=DEV)
+            tc.reduce_tensor(g, K, T, got, op)
+            tc.reduce(g, copies, sep, op)
+            torch.cuda.synchronize()
+            assert_bits_equal(host_f32(got), host_f32(sep), f"K={K} {name} {op}: tensor vs separate")
+            if name == "integer" and op == "sum":
+                assert_exact(host_f32(got), orc.reduce(orc.copies_from_tensor(host, K, N), code), f"K={K} sum")
+
+
 @pytest.mark.parametrize("K", [1, 3, 8, 16, 31, 64])
 def test_tensor_integer_inputs_bit_exact(orc, K):
     """Exact regime (integers, eta = 1/8, rho = 1/2): bit for bit."""
