@@ -497,7 +497,8 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
     constexpr int ROW = (P + 1) * SB;               // padded tile row, bytes
     __shared__ int32_t s_rel[kMaxStage + 1];
     __shared__ uintptr_t s_base[kMaxStage];
-    __shared__ __attribute__((aligned(16))) unsigned char s_tile[M * ROW];
+    // one row more than a tile: unpack keeps the next tile's first slot there
+    __shared__ __attribute__((aligned(16))) unsigned char s_tile[(M + 1) * ROW];
     const int K = a.K;
     const int64_t cstart = static_cast<int64_t>(blockIdx.x) * a.chunk;
     const int32_t clen = static_cast<int32_t>(a.N - cstart < a.chunk ? a.N - cstart : a.chunk);
@@ -535,6 +536,10 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
     };
     auto tile = [&](int jl, int kk) -> unsigned char* { return s_tile + jl * ROW + kk * SB; };
     const int nsl = clen / 4;  // whole slots in this chunk
+    // a lane's slot is the same in every pass of the unpack's scatter (the
+    // binary32 scatter finds its tensor once; for 8-byte slots the extra live
+    // registers cost more than the search)
+    constexpr bool kSame = SB == 16 && 256 % M == 0;
     if constexpr (DIRECT) {
         // a slot-aligned group and list: lanes take the pieces in tensor order
         // (P per slot, lane i = copy i) and move each slot straight between
@@ -641,8 +646,14 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                 else gst_nt<u2>(piece(t0 + jl, kk), *reinterpret_cast<const u2*>(tile(jl, kk)));
             }
         } else {
-            // tensor -> tile, in tensor order
+            // tensor -> tile, in tensor order.  With a full tile before the
+            // chunk's last whole slot, the first K lanes also load the next
+            // tile's first slot into the extra row, where the funnel of a
+            // misaligned destination's last granule in this tile finds it.
             u4 v[R];
+            const bool ahead = SB == 16 && threadIdx.x < K && mt == M && t0 + M < nsl;
+            u4 nx = u4{0u, 0u, 0u, 0u};
+            if (ahead) nx = gld<u4>(piece(t0 + M, threadIdx.x));
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const int q = threadIdx.x + r * 256;
@@ -655,6 +666,7 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                     v[r] = u4{w.x, w.y, 0u, 0u};
                 }
             }
+            if (ahead) *reinterpret_cast<u4*>(tile(M, threadIdx.x)) = nx;
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const int q = threadIdx.x + r * 256;
@@ -664,14 +676,16 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                 else *reinterpret_cast<u2*>(tile(jl, kk)) = u2{v[r].x, v[r].y};
             }
             __syncthreads();
-            // tile -> copies: lanes walk consecutive slots of one copy
+            // tile -> copies: lanes walk consecutive slots of one copy (the
+            // same slot in every pass when M divides 256)
+            const int s_same = kSame && threadIdx.x % M < mt ? find(4 * (t0 + threadIdx.x % M)) : 0;
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const int q = threadIdx.x + r * 256;
                 const int kk = q / M, jl = q % M;
                 if (kk >= K || jl >= mt) continue;
                 const int js = t0 + jl, jr = 4 * js;
-                int s = find(jr);
+                int s = kSame ? s_same : find(jr);
                 const int32_t r1 = rel(s + 1);
                 const T* src = reinterpret_cast<const T*>(tile(jl, kk));
                 if (jr + 4 <= r1) {
@@ -686,8 +700,9 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                         if (js == run_lo)  // bytes before the first granule
                             for (uint32_t e = 0; e < sh / ES; ++e) gst<T>(w + e * ES, src[e]);
                         if (js + 1 < run_hi) {
-                            const u4 next = jl + 1 < mt ? *reinterpret_cast<const u4*>(tile(jl + 1, kk))
-                                                        : load_bytes<SB>(piece(js + 1, kk));
+                            // slot js + 1 is a whole slot of the chunk: row jl + 1
+                            // of this tile, or the extra row (jl + 1 = mt = M)
+                            const u4 next = *reinterpret_cast<const u4*>(tile(jl + 1, kk));
                             gst_nt<u4>(G, funnel(*reinterpret_cast<const u4*>(src), next, sh));
                         } else {  // the last whole slot: bytes after G
                             for (uint32_t e = sh / ES; e < 4; ++e) gst<T>(w + e * ES, src[e]);
