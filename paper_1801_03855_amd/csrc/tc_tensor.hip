@@ -783,11 +783,18 @@ constexpr int kPipeStage = 512;
 // TILE/256 pieces each.  The straight path (no LDS) holds them in registers;
 // the tiled path stages them in LDS, where smaller tiles leave room for more
 // workgroups per CU (measured on MI355X: 1024 and 512 best respectively).
+// At P >= 16 a tile of 512 pieces holds only 32 slots of each copy, and
+// 1024 pieces measure better: the 10,000-tensor bfloat16 group at K = 16
+// 4.39 -> 4.56 TB/s, ResNet-50 at K = 16 level or better; 2048 fell to 3.5
+// on the 10,000-tensor group, and at P = 8 512 stays best.
 #ifndef TC_PIPE_TILE
 #define TC_PIPE_TILE 1024
 #endif
 #ifndef TC_PIPE_TILE_LDS
 #define TC_PIPE_TILE_LDS 512
+#endif
+#ifndef TC_PIPE_TILE_LDS_WIDE
+#define TC_PIPE_TILE_LDS_WIDE 1024
 #endif
 
 
@@ -803,7 +810,7 @@ template <int P, typename T, bool WG, typename I, bool DIRECT>
 __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
     constexpr int ES = sizeof(T);
     constexpr int SB = 4 * ES;                         // gradient slot bytes
-    constexpr int TILE = DIRECT ? TC_PIPE_TILE : TC_PIPE_TILE_LDS;
+    constexpr int TILE = DIRECT ? TC_PIPE_TILE : P >= 16 ? TC_PIPE_TILE_LDS_WIDE : TC_PIPE_TILE_LDS;
     constexpr int M = TILE / P > 16 ? TILE / P : 16;  // slots per tile
     constexpr int R = (M * P) / 256;                                 // pieces per lane and phase
     constexpr int ROWG = (P + 1) * SB, ROWX = (P + 1) * 16;
@@ -1245,9 +1252,21 @@ hipError_t run_tpipe(const TPipeArgs& a, unsigned blocks, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// The straight path pays only while a wave moves at least 128 contiguous
+// bytes of every copy's gradient tensors: (64 / P) slots of 4 elements.
+// Measured on ResNet-50 and VGG-16 groups: at P = 16 binary32 it ran at 3.9
+// against 5.0 TB/s tiled, at P = 8 bfloat16 at 5.0 against 5.2, and 3 to 7
+// times slower at P = 32 and 64; within the bound it is 3-7% ahead.
+template <int P, typename T>
+constexpr bool pipe_direct_pays() { return (64 / P) * 4 * static_cast<int>(sizeof(T)) >= 128; }
+
 template <int P, typename T>
 hipError_t run_tpipe(const TPipeArgs& a, bool direct, unsigned blocks, hipStream_t stream) {
-    hipError_t e = direct ? run_tpipe<P, T, true>(a, blocks, stream) : run_tpipe<P, T, false>(a, blocks, stream);
+    hipError_t e;
+    if constexpr (pipe_direct_pays<P, T>())
+        e = direct ? run_tpipe<P, T, true>(a, blocks, stream) : run_tpipe<P, T, false>(a, blocks, stream);
+    else
+        e = run_tpipe<P, T, false>(a, blocks, stream);
     if (e != hipSuccess || a.N % 4 == 0) return e;
     if (a.gt) hipLaunchKernelGGL((tensor_pipeline_tail_kernel<P, T, true>), dim3(1), dim3(64), 0, stream, a);
     else hipLaunchKernelGGL((tensor_pipeline_tail_kernel<P, T, false>), dim3(1), dim3(64), 0, stream, a);
@@ -1263,7 +1282,8 @@ hipError_t launch_tensor_pipeline(const tc_tensorlist* grads, const tc_tensorlis
     const bool bf16 = grads->elem == 2;
     // straight between registers and the per-layer tensors when every tensor
     // boundary before the last, partial slot falls on a slot boundary and
-    // every tensor of both lists is slot-aligned
+    // every tensor of both lists is slot-aligned (and K is small enough,
+    // pipe_direct_pays)
     const bool direct = g->slot_bounds && grads->slot_aligned && params->slot_aligned;
     switch (next_pow2(grads->K)) {
 #define TC_CASE(p) \

@@ -181,15 +181,20 @@ def test_misaligned_tensors(orc, K, gdt):
     _run(orc, sizes, K, gdt=gdt, seed=10 + K, misalign=True)
 
 
-@pytest.mark.parametrize("K", [1, 2, 3, 5, 8, 16, 33, 64])
-def test_slot_aligned_groups(orc, K):
+@pytest.mark.parametrize("K,gdt", [(1, torch.float32), (2, torch.float32), (3, torch.float32),
+                                   (5, torch.float32), (8, torch.float32), (16, torch.float32),
+                                   (33, torch.float32), (64, torch.float32), (2, torch.bfloat16),
+                                   (4, torch.bfloat16), (8, torch.bfloat16), (16, torch.bfloat16)])
+def test_slot_aligned_groups(orc, K, gdt):
     """Every tensor boundary before the last slot on a slot boundary and
-    every tensor slot-aligned: the kernel moves each chunk straight between
-    registers and the per-layer tensors; the last tensor ends inside a slot,
-    which a launch of its own completes."""
+    every tensor slot-aligned: while a wave still moves 128 contiguous bytes
+    of each copy's gradients (K <= 8 binary32, K <= 4 bfloat16) the kernel
+    moves each chunk straight between registers and the per-layer tensors,
+    beyond that through the tiles; the last tensor ends inside a slot, which
+    a launch of its own completes."""
     sizes = [4096, 8, 0, 12000, 516, 7]
-    _run(orc, sizes, K, seed=70 + K)
-    _run(orc, sizes, K, seed=80 + K, eta=0.125, rho=0.5, integer=True)
+    _run(orc, sizes, K, gdt=gdt, seed=70 + K)
+    _run(orc, sizes, K, gdt=gdt, seed=80 + K, eta=0.125, rho=0.5, integer=True)
 
 
 @pytest.mark.parametrize("gdt", [torch.float32, torch.bfloat16])
