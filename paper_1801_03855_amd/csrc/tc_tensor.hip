@@ -481,9 +481,15 @@ __device__ __forceinline__ void store_bytes(uintptr_t D, u4 v) {
 //           last one the bytes after it (binary32; an unaligned bfloat16
 //           slot is stored element by element).
 // A slot spanning two tensors moves element by element.
-// Pieces (one slot of one copy) per LDS tile of the pack and unpack.
+// Pieces (one slot of one copy) per LDS tile of the pack and unpack.  The
+// binary32 unpack at P >= 16 takes twice as many (measured on MI355X: the
+// 10,000-tensor group at K = 16 4.21 -> 4.49 TB/s, ResNet-50 at K = 16 and
+// 32 level); pack loses 4-13% with them at every K measured.
 #ifndef TC_TPACK_TILE
 #define TC_TPACK_TILE 1024
+#endif
+#ifndef TC_TUNPACK_TILE_WIDE
+#define TC_TUNPACK_TILE_WIDE 2048
 #endif
 #ifndef TC_TPACK_DIRECT
 #define TC_TPACK_DIRECT 1
@@ -493,7 +499,8 @@ template <int P, typename T, bool UNPACK, bool DIRECT>
 __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
     constexpr int ES = sizeof(T);
     constexpr int SB = 4 * ES;                      // slot bytes
-    constexpr int M = TC_TPACK_TILE / P > 16 ? TC_TPACK_TILE / P : 16;  // slots per LDS tile
+    constexpr int TILE = UNPACK && ES == 4 && P >= 16 ? TC_TUNPACK_TILE_WIDE : TC_TPACK_TILE;
+    constexpr int M = TILE / P > 16 ? TILE / P : 16;  // slots per LDS tile
     constexpr int ROW = (P + 1) * SB;               // padded tile row, bytes
     __shared__ int32_t s_rel[kMaxStage + 1];
     __shared__ uintptr_t s_base[kMaxStage];
