@@ -385,25 +385,40 @@ def test_resnet50_k8_100_iterations_every_path(orc):
     assert_close(host_f32(xc[ti]), rc, mc, "x_c after 100 steps")
 
 
-def test_steps_replay_from_a_hip_graph():
+@pytest.mark.parametrize("case", ["tiny_k2", "misaligned_k3_bf16"])
+def test_steps_replay_from_a_hip_graph(case):
     """Every data entry point only launches kernels (no allocation, no
     synchronisation, no memset), so a step can be captured in a HIP graph.
     The four calls and the one-launch pipeline are captured once and
     replayed five times, with eager work and synchronisations between the
     replays; after every replay the state equals the same number of eager
-    steps, bit for bit."""
-    w = wl.WORKLOADS["tiny_k2"]
-    sizes = w.sizes()
-    g = tc.Group(sizes)
-    N, K = g.numel, w.K
-    gflat = wl.make_gradients(w, N, DEV)
-    xs, xc = wl.make_state(w, N, DEV)
-    grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gflat])
+    steps, bit for bit.  The tiny group takes the straight paths; the
+    second case (lengths not multiples of 4, bfloat16 gradient tensors one
+    element into their buffer, a ragged tail) the tiles, funnel shifts and
+    the pipeline's tail launch."""
+    if case == "tiny_k2":
+        w = wl.WORKLOADS["tiny_k2"]
+        sizes, K, gdt, eta, rho = w.sizes(), w.K, torch.float32, w.eta, w.rho
+        g = tc.Group(sizes)
+        N = g.numel
+        gflat = wl.make_gradients(w, N, DEV)
+        xs, xc = wl.make_state(w, N, DEV)
+        grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gflat])
+    else:
+        sizes, K, gdt, eta, rho = [513, 4099, 6, 7001, 3], 3, torch.bfloat16, 0.05, 2.0
+        g = tc.Group(sizes)
+        N = g.numel
+        gen = torch.Generator(device=DEV).manual_seed(77)
+        gflat = [(torch.randn(N + 1, generator=gen, device=DEV) * 0.01).to(gdt)[1:] for _ in range(K)]
+        xs = [torch.randn(N, generator=gen, device=DEV) * 0.05 for _ in range(K)]
+        xc = torch.randn(N, generator=gen, device=DEV) * 0.05
+        grads = tc.TensorList(g, [wl.split_views(f, sizes) for f in gflat])
 
     def make():
-        X = torch.empty(tc.tensor_numel(g, K), device=DEV)
+        # zeros: the padding of a partial last slot is never written
+        X = torch.zeros(tc.tensor_numel(g, K), device=DEV)
         tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
-        G = torch.empty(tc.tensor_numel(g, K), device=DEV)
+        G = torch.zeros(tc.tensor_numel(g, K), dtype=gdt, device=DEV)
         params = [torch.empty(N, device=DEV) for _ in range(K)]
         return dict(X=X, G=G, c=xc.clone(), gbar=torch.empty(N, device=DEV), params=params,
                     ptl=tc.TensorList(g, [wl.split_views(p, sizes) for p in params]))
@@ -411,11 +426,11 @@ def test_steps_replay_from_a_hip_graph():
     def four(st, s):
         tc.pack_tensor(grads, st["G"], s)
         tc.reduce_tensor(g, K, st["G"], st["gbar"], "avg", s)
-        tc.easgd_step_tensor(g, K, st["X"], st["G"], st["c"], w.eta, w.rho, s)
+        tc.easgd_step_tensor(g, K, st["X"], st["G"], st["c"], eta, rho, s)
         tc.unpack_tensor(st["ptl"], st["X"], s)
 
     def one(st, s):
-        tc.easgd_pipeline_tensor(grads, st["ptl"], st["G"], st["gbar"], st["X"], st["c"], w.eta, w.rho, s)
+        tc.easgd_pipeline_tensor(grads, st["ptl"], st["G"], st["gbar"], st["X"], st["c"], eta, rho, s)
 
     for step in (four, one):
         eager, graphed = make(), make()
