@@ -368,6 +368,67 @@ def _time_launches(fns, reps):
     return t[reps // 2], t[0]
 
 
+def graph_step_rows(tc, wl, reps=200):
+    """The tiny group's whole step (pack, AVG, fused step, unpack on the
+    tensor layout; and the same as one easgd_pipeline_tensor launch), timed
+    over reps back-to-back steps: issued eagerly, and replayed from a HIP
+    graph captured once.  A group this small is bound by launch and
+    host-call overhead, which the graph removes."""
+    import torch
+
+    w = wl.WORKLOADS["tiny_k2"]
+    sizes = w.sizes()
+    g = tc.Group(sizes)
+    N, K, dev = g.numel, w.K, "cuda"
+    gs = wl.make_gradients(w, N, dev)
+    xs, xc = wl.make_state(w, N, dev)
+    grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gs])
+    params = tc.TensorList(g, [[torch.empty(n, device=dev) for n in sizes] for _ in range(K)])
+    X = torch.zeros(tc.tensor_numel(g, K), device=dev)
+    tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
+    G = torch.zeros(tc.tensor_numel(g, K), device=dev)
+    gbar = torch.empty(N, device=dev)
+
+    def four(s):
+        tc.pack_tensor(grads, G, s)
+        tc.reduce_tensor(g, K, G, gbar, "avg", s)
+        tc.easgd_step_tensor(g, K, X, G, xc, w.eta, w.rho, s)
+        tc.unpack_tensor(params, X, s)
+
+    def one(s):
+        tc.easgd_pipeline_tensor(grads, params, G, gbar, X, xc, w.eta, w.rho, s)
+
+    def per_step(fn):
+        stream = torch.cuda.current_stream()
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    out = {"workload": "tiny group, K = 2, tensor layout", "N": N, "K": K}
+    for name, step in (("four calls", four), ("one launch", one)):
+        eager = per_step(lambda: step(torch.cuda.current_stream()))
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            step(side)
+        torch.cuda.synchronize()
+        replay = per_step(graph.replay)
+        out[name] = {"eager_ms": round(eager, 5), "graph_ms": round(replay, 5),
+                     "eager_steps_per_s": round(1e3 / eager, 1), "graph_steps_per_s": round(1e3 / replay, 1)}
+        del graph
+    torch.cuda.synchronize()
+    return out
+
+
 def config_table(tc, wl, reps=20):
     """Every configured workload's operations on both layouts: median and
     minimum time of single launches, algorithmic GB/s at the median and its
@@ -594,6 +655,7 @@ def main():
     configs = None
     if not args.no_configs:
         configs = config_table(tc, wl)
+        configs["tiny_k2"]["whole step, eager and HIP graph"] = graph_step_rows(tc, wl)
 
     extra = None
     if not args.no_next_rows and args.workload == "resnet50_k8_pipeline":
