@@ -121,6 +121,26 @@ def recorded_traffic(workload: str, layout: str):
     return {k[len("traffic_bytes_"):]: int(v) for k, v in vals.items() if k.startswith("traffic_bytes_")}
 
 
+def host_cpu() -> dict:
+    """The host the oracle runs on: CPU model, sockets, logical CPUs, and the
+    CPUs this process may use."""
+    model, sockets = "unknown", set()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                key, _, val = line.partition(":")
+                key, val = key.strip(), val.strip()
+                if key == "model name" and model == "unknown":
+                    model = val
+                elif key == "physical id":
+                    sockets.add(val)
+    except OSError:
+        pass
+    usable = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {"cpu_model": model, "sockets": len(sockets) or None, "logical_cpus": os.cpu_count(),
+            "usable_cpus": usable}
+
+
 def cpu_baseline(wkey: str, ops, sample_elems: int = 30_000_000, min_seconds: float = 10.0,
                  max_reps: int = 20):
     """The oracle, as it is, on the first tensors of the group (at least
@@ -174,14 +194,15 @@ def cpu_baseline(wkey: str, ops, sample_elems: int = 30_000_000, min_seconds: fl
            "sample": f"{reps} passes of {'+'.join(ops)} over the first {len(sub)} tensors of the group "
                      f"({n} elements, K={w.K}); binary64 C oracle, 1 thread",
            "seconds": round(secs, 3),
-           "steps_per_s": round(reps * n / (secs * sum(sizes)), 4)}
+           "steps_per_s": round(reps * n / (secs * sum(sizes)), 4),
+           "host": host_cpu()}
 
     # the same oracle functions on every host core: each thread takes a
     # contiguous block of whole tensors through the four operations (the
     # operations are elementwise, so the blocks never share an element)
     from concurrent.futures import ThreadPoolExecutor
 
-    threads = max(1, min(16, os.cpu_count() or 1))
+    threads = max(1, min(16, out["host"]["usable_cpus"] or 1))
     offs = np.cumsum([0] + sub)
     bounds = [int(np.searchsorted(offs, n * j / threads)) for j in range(threads)] + [len(sub)]
     blocks = [(a, b) for a, b in zip(bounds[:-1], bounds[1:]) if b > a]

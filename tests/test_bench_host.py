@@ -87,3 +87,10 @@ def test_source_hash_ignores_comments_only(tmp_path, monkeypatch):
     assert bench.kernel_source_sha() != h0
     src.write_text('int f() { return 1; } // one\n/* two */ const char* s = "a // c";\n')
     assert bench.kernel_source_sha() != h0
+
+
+def test_host_cpu_description():
+    h = bench.host_cpu()
+    assert h["logical_cpus"] and h["logical_cpus"] >= 1
+    assert h["usable_cpus"] and 1 <= h["usable_cpus"] <= h["logical_cpus"]
+    assert isinstance(h["cpu_model"], str) and h["cpu_model"]
