@@ -84,38 +84,46 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         g->offsets[t + 1] = g->offsets[t] + sizes[t];
     }
     g->N = g->offsets[n];
-    g->chunk = g->N / n >= TC_PACK_LARGE_MEAN ? TC_PACK_CHUNK_LARGE : TC_PACK_CHUNK_SMALL;
-    g->nchunks = (g->N + g->chunk - 1) / g->chunk;
-    if (g->nchunks > INT32_MAX / 2) { set_error("group too large"); delete g; return nullptr; }
-    // chunk_first[b]: the tensor holding flat position b*chunk, i.e. the
-    // last tensor whose offset is <= that position (zero-size tensors at the
-    // same offset come before the one that holds it).  The final entry is
-    // the tensor holding position N-1.
-    g->chunk_first.resize(static_cast<size_t>(g->nchunks) + 1);
+    const bool large = g->N / n >= TC_PACK_LARGE_MEAN;
+    g->sep.chunk = large ? TC_PACK_CHUNK_LARGE : TC_PACK_CHUNK_SMALL;
+    g->tpack.chunk = TC_TPACK_CHUNK;
+    g->pipe.chunk = TC_PIPE_CHUNK;
+    // first[b]: the tensor holding flat position b*chunk, i.e. the last
+    // tensor whose offset is <= that position (zero-size tensors at the same
+    // offset come before the one that holds it).  The final entry is the
+    // tensor holding position N-1.
     auto tensor_at = [&](int64_t j) {
         auto it = std::upper_bound(g->offsets.begin(), g->offsets.begin() + n, j);
         return static_cast<int32_t>(it - g->offsets.begin()) - 1;
     };
-    for (int64_t b = 0; b < g->nchunks; ++b) g->chunk_first[b] = tensor_at(b * g->chunk);
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->pipe}) {
+        c->nchunks = (g->N + c->chunk - 1) / c->chunk;
+        if (c->nchunks > INT32_MAX / 2) { set_error("group too large"); delete g; return nullptr; }
+        c->first.resize(static_cast<size_t>(c->nchunks) + 1);
+        for (int64_t b = 0; b < c->nchunks; ++b) c->first[b] = tensor_at(b * c->chunk);
+        c->first[c->nchunks] = g->N > 0 ? tensor_at(g->N - 1) : 0;
+    }
     g->slot_bounds = true;
     for (int32_t t = 1; t < n; ++t)
         if (g->offsets[t] % 4 != 0 && g->offsets[t] < g->N / 4 * 4) g->slot_bounds = false;
-    g->chunk_first[g->nchunks] = g->N > 0 ? tensor_at(g->N - 1) : 0;
 
     hipError_t e = hipGetDevice(&g->device);
     if (e != hipSuccess) { hip_fail(e, "hipGetDevice"); delete g; return nullptr; }
-    size_t ob = g->offsets.size() * sizeof(int64_t), cb = g->chunk_first.size() * sizeof(int32_t);
+    size_t ob = g->offsets.size() * sizeof(int64_t);
     if ((e = hipMalloc(&g->d_offsets, ob)) != hipSuccess ||
-        (e = hipMalloc(&g->d_chunk_first, cb)) != hipSuccess) {
-        hip_fail(e, "hipMalloc (group tables)");
+        (e = hipMemcpy(g->d_offsets, g->offsets.data(), ob, hipMemcpyHostToDevice)) != hipSuccess) {
+        hip_fail(e, "group offset table");
         tc_group_destroy(g);
         return nullptr;
     }
-    if ((e = hipMemcpy(g->d_offsets, g->offsets.data(), ob, hipMemcpyHostToDevice)) != hipSuccess ||
-        (e = hipMemcpy(g->d_chunk_first, g->chunk_first.data(), cb, hipMemcpyHostToDevice)) != hipSuccess) {
-        hip_fail(e, "hipMemcpy (group tables)");
-        tc_group_destroy(g);
-        return nullptr;
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->pipe}) {
+        const size_t cb = c->first.size() * sizeof(int32_t);
+        if ((e = hipMalloc(&c->d_first, cb)) != hipSuccess ||
+            (e = hipMemcpy(c->d_first, c->first.data(), cb, hipMemcpyHostToDevice)) != hipSuccess) {
+            hip_fail(e, "group chunk table");
+            tc_group_destroy(g);
+            return nullptr;
+        }
     }
     return g;
 }
@@ -123,7 +131,8 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
 TC_API void tc_group_destroy(tc_group* g) {
     if (!g) return;
     if (g->d_offsets) (void)hipFree(g->d_offsets);
-    if (g->d_chunk_first) (void)hipFree(g->d_chunk_first);
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->pipe})
+        if (c->d_first) (void)hipFree(c->d_first);
     delete g;
 }
 

@@ -12,17 +12,32 @@
 
 namespace tc {
 
-// Elements per pack/unpack chunk; one workgroup gathers or scatters one
-// chunk of one copy.  Chosen per group from its mean tensor size: groups of
-// large tensors (almost every chunk inside one tensor) move best in short
-// chunks that a workgroup covers in one batch per lane; groups of many small
-// tensors in long chunks, which spread the per-chunk segment staging over
-// more data (measured on MI355X).  Multiples of every vector width (4, 8).
+// Elements per chunk: one workgroup takes one chunk (of one copy, on
+// separate buffers; of all K copies, on the tensor layout).  Each kind of
+// kernel cuts the group its own way, chosen from the group's mean tensor
+// size (measured on MI355X):
+// - separate-buffer pack/unpack: groups of large tensors (almost every chunk
+//   inside one tensor) move best in short chunks that a workgroup covers in
+//   one batch per lane; groups of many small tensors in longer chunks, which
+//   spread the per-chunk segment staging over more data (4,096: pack plus
+//   unpack 4% faster than with 8,192, 10% faster than with 2,048);
+// - tensor-layout pack/unpack, whose workgroups move all K copies of a chunk:
+//   1,024 elements (against 2,048 and 512 on ResNet-50 and VGG-16, and
+//   against 2,048 to 8,192 on 10,000 small tensors);
+// - the pipelined step: 512 elements (7-8% faster than 2,048 on ResNet-50,
+//   VGG-16 and 10,000 small tensors; 2% faster than 1,024 on the latter).
+// All are multiples of every vector width (4, 8).
 #ifndef TC_PACK_CHUNK_LARGE
 #define TC_PACK_CHUNK_LARGE 2048
 #endif
 #ifndef TC_PACK_CHUNK_SMALL
-#define TC_PACK_CHUNK_SMALL 8192
+#define TC_PACK_CHUNK_SMALL 4096
+#endif
+#ifndef TC_TPACK_CHUNK
+#define TC_TPACK_CHUNK 1024
+#endif
+#ifndef TC_PIPE_CHUNK
+#define TC_PIPE_CHUNK 512
 #endif
 #ifndef TC_PACK_LARGE_MEAN
 #define TC_PACK_LARGE_MEAN 32768
@@ -96,21 +111,29 @@ hipError_t launch_tensor_pipeline(const tc_tensorlist* grads, const tc_tensorlis
 
 }  // namespace tc
 
+// One cut of the flat index space into chunks of `chunk` elements (the last
+// one shorter) with, per chunk, the first tensor it touches.
+struct tc_chunking {
+    int64_t chunk = 0;           // elements per chunk
+    int64_t nchunks = 0;         // ceil(N / chunk)
+    std::vector<int32_t> first;  // nchunks + 1
+    int32_t* d_first = nullptr;  // device copy
+};
+
 // Group descriptor: host copies of sizes and offsets, and device copies of
-// the offset table and of the per-chunk first-segment table.
+// the offset table and of each chunking's first-segment table.
 struct tc_group {
     int32_t n = 0;
     int64_t N = 0;
     int device = 0;
     std::vector<int64_t> sizes;
-    std::vector<int64_t> offsets;      // n + 1
-    int64_t chunk = 0;                 // elements per pack/unpack chunk
-    int64_t nchunks = 0;               // ceil(N / chunk)
-    std::vector<int32_t> chunk_first;  // nchunks + 1
-    bool slot_bounds = false;          // every tensor boundary before the last,
-                                       // partial slot is a multiple of 4
+    std::vector<int64_t> offsets;  // n + 1
+    tc_chunking sep;               // separate-buffer pack/unpack
+    tc_chunking tpack;             // tensor-layout pack/unpack
+    tc_chunking pipe;              // the pipelined step
+    bool slot_bounds = false;      // every tensor boundary before the last,
+                                   // partial slot is a multiple of 4
     int64_t* d_offsets = nullptr;
-    int32_t* d_chunk_first = nullptr;
 };
 
 // K copies of a group held as separate tensors: device table of K*n

@@ -251,17 +251,17 @@ hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, 
     const tc_group* g = tl->g;
     PackKernelArgs a{};
     a.offsets = g->d_offsets;
-    a.chunk_first = g->d_chunk_first;
+    a.chunk_first = g->sep.d_first;
     a.ptrs = tl->d_ptrs;
     a.n = g->n;
     a.N = g->N;
-    a.chunk = g->chunk;
+    a.chunk = g->sep.chunk;
     for (int k = 0; k < tl->K; ++k) a.flat[k] = flat[k];
     if (tl->elem == 2)
-        return unpack ? run<uint16_t, true>(a, tl->K, g->nchunks, stream)
-                      : run<uint16_t, false>(a, tl->K, g->nchunks, stream);
-    return unpack ? run<uint32_t, true>(a, tl->K, g->nchunks, stream)
-                  : run<uint32_t, false>(a, tl->K, g->nchunks, stream);
+        return unpack ? run<uint16_t, true>(a, tl->K, g->sep.nchunks, stream)
+                      : run<uint16_t, false>(a, tl->K, g->sep.nchunks, stream);
+    return unpack ? run<uint32_t, true>(a, tl->K, g->sep.nchunks, stream)
+                  : run<uint32_t, false>(a, tl->K, g->sep.nchunks, stream);
 }
 
 }  // namespace tc

@@ -1227,8 +1227,8 @@ hipError_t run_tpack(const TPackArgs& a, int elem, bool unpack, unsigned blocks,
 
 hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStream_t stream) {
     const tc_group* g = tl->g;
-    TPackArgs a{g->d_offsets, g->d_chunk_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, g->chunk};
-    const unsigned blocks = static_cast<unsigned>(g->nchunks);
+    TPackArgs a{g->d_offsets, g->tpack.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, g->tpack.chunk};
+    const unsigned blocks = static_cast<unsigned>(g->tpack.nchunks);
     // straight through registers when every tensor boundary before the last,
     // partial slot falls on a slot boundary, every tensor of the list is
     // slot-aligned and a wave still moves >= 256 contiguous bytes of each copy
@@ -1283,9 +1283,9 @@ hipError_t run_tpipe(const TPipeArgs& a, bool direct, unsigned blocks, hipStream
 hipError_t launch_tensor_pipeline(const tc_tensorlist* grads, const tc_tensorlist* params, void* gt, float* gbar,
                                   float* x, float* xc, float eta, float rho, hipStream_t stream) {
     const tc_group* g = grads->g;
-    TPipeArgs a{g->d_offsets, g->d_chunk_first, grads->d_ptrs, params->d_ptrs, gt, gbar, x, xc,
-                g->n, grads->K, g->N, g->chunk, eta, rho, eta * rho};
-    const unsigned blocks = static_cast<unsigned>(g->nchunks);
+    TPipeArgs a{g->d_offsets, g->pipe.d_first, grads->d_ptrs, params->d_ptrs, gt, gbar, x, xc,
+                g->n, grads->K, g->N, g->pipe.chunk, eta, rho, eta * rho};
+    const unsigned blocks = static_cast<unsigned>(g->pipe.nchunks);
     const bool bf16 = grads->elem == 2;
     // straight between registers and the per-layer tensors when every tensor
     // boundary before the last, partial slot falls on a slot boundary and

@@ -117,7 +117,9 @@ def test_pack_tensor_views_and_many_small(orc, dtype):
     _tensor_pack_roundtrip(orc, [1, 2, 3, 5, 8, 13, 4099, 1, 7, 4096, 0, 9001], 4, dtype, seed=5, views=True)
     _tensor_pack_roundtrip(orc, wl.many_small_sizes(1500, seed=9), 16, dtype, seed=6, misalign=True)
     rng = np.random.default_rng(4)
-    _tensor_pack_roundtrip(orc, rng.integers(0, 4, 3000).tolist(), 2, dtype, seed=7)  # > 1024 per chunk
+    # tensors of 0 or 1 elements: about 2,000 per 1,024-element chunk, more than
+    # the LDS tables hold, so the global-table search runs too
+    _tensor_pack_roundtrip(orc, rng.integers(0, 2, 6000).tolist(), 2, dtype, seed=7)
 
 
 # ------------------------------------------------------------------ reduce
