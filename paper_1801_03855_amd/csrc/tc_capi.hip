@@ -84,9 +84,10 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         g->offsets[t + 1] = g->offsets[t] + sizes[t];
     }
     g->N = g->offsets[n];
-    const bool large = g->N / n >= TC_PACK_LARGE_MEAN;
-    g->sep.chunk = large ? TC_PACK_CHUNK_LARGE : TC_PACK_CHUNK_SMALL;
+    g->large = g->N / n >= TC_PACK_LARGE_MEAN;
+    g->sep.chunk = g->large ? TC_PACK_CHUNK_LARGE : TC_PACK_CHUNK_SMALL;
     g->tpack.chunk = TC_TPACK_CHUNK;
+    g->tpack_fine.chunk = TC_TPACK_CHUNK_FINE;
     g->pipe.chunk = TC_PIPE_CHUNK;
     // first[b]: the tensor holding flat position b*chunk, i.e. the last
     // tensor whose offset is <= that position (zero-size tensors at the same
@@ -96,7 +97,7 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         auto it = std::upper_bound(g->offsets.begin(), g->offsets.begin() + n, j);
         return static_cast<int32_t>(it - g->offsets.begin()) - 1;
     };
-    for (tc_chunking* c : {&g->sep, &g->tpack, &g->pipe}) {
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe}) {
         c->nchunks = (g->N + c->chunk - 1) / c->chunk;
         if (c->nchunks > INT32_MAX / 2) { set_error("group too large"); delete g; return nullptr; }
         c->first.resize(static_cast<size_t>(c->nchunks) + 1);
@@ -116,7 +117,7 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         tc_group_destroy(g);
         return nullptr;
     }
-    for (tc_chunking* c : {&g->sep, &g->tpack, &g->pipe}) {
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe}) {
         const size_t cb = c->first.size() * sizeof(int32_t);
         if ((e = hipMalloc(&c->d_first, cb)) != hipSuccess ||
             (e = hipMemcpy(c->d_first, c->first.data(), cb, hipMemcpyHostToDevice)) != hipSuccess) {
@@ -131,7 +132,7 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
 TC_API void tc_group_destroy(tc_group* g) {
     if (!g) return;
     if (g->d_offsets) (void)hipFree(g->d_offsets);
-    for (tc_chunking* c : {&g->sep, &g->tpack, &g->pipe})
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe})
         if (c->d_first) (void)hipFree(c->d_first);
     delete g;
 }

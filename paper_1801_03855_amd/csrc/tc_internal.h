@@ -22,8 +22,10 @@ namespace tc {
 //   spread the per-chunk segment staging over more data (4,096: pack plus
 //   unpack 4% faster than with 8,192, 10% faster than with 2,048);
 // - tensor-layout pack/unpack, whose workgroups move all K copies of a chunk:
-//   1,024 elements (against 2,048 and 512 on ResNet-50 and VGG-16, and
-//   against 2,048 to 8,192 on 10,000 small tensors);
+//   1,024 elements (against 2,048 and 512 on VGG-16's straight path, and
+//   against 512 and 2,048 to 8,192 on 10,000 small tensors), but 512 for
+//   the unpack through the tiles on groups of large tensors (ResNet-50:
+//   4-5% faster at K = 8, 8% at K = 16; the pack is 3% slower there);
 // - the pipelined step: 512 elements (7-8% faster than 2,048 on ResNet-50,
 //   VGG-16 and 10,000 small tensors; 2% faster than 1,024 on the latter).
 // All are multiples of every vector width (4, 8).
@@ -35,6 +37,9 @@ namespace tc {
 #endif
 #ifndef TC_TPACK_CHUNK
 #define TC_TPACK_CHUNK 1024
+#endif
+#ifndef TC_TPACK_CHUNK_FINE
+#define TC_TPACK_CHUNK_FINE 512
 #endif
 #ifndef TC_PIPE_CHUNK
 #define TC_PIPE_CHUNK 512
@@ -128,8 +133,10 @@ struct tc_group {
     int device = 0;
     std::vector<int64_t> sizes;
     std::vector<int64_t> offsets;  // n + 1
+    bool large = false;            // mean tensor size >= TC_PACK_LARGE_MEAN
     tc_chunking sep;               // separate-buffer pack/unpack
     tc_chunking tpack;             // tensor-layout pack/unpack
+    tc_chunking tpack_fine;        // unpack through the tiles, large tensors
     tc_chunking pipe;              // the pipelined step
     bool slot_bounds = false;      // every tensor boundary before the last,
                                    // partial slot is a multiple of 4

@@ -1227,14 +1227,17 @@ hipError_t run_tpack(const TPackArgs& a, int elem, bool unpack, unsigned blocks,
 
 hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStream_t stream) {
     const tc_group* g = tl->g;
-    TPackArgs a{g->d_offsets, g->tpack.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, g->tpack.chunk};
-    const unsigned blocks = static_cast<unsigned>(g->tpack.nchunks);
     // straight through registers when every tensor boundary before the last,
     // partial slot falls on a slot boundary, every tensor of the list is
     // slot-aligned and a wave still moves >= 256 contiguous bytes of each copy
     // (P <= 4): measured on MI355X, VGG-16 at K = 4 packs 5% faster that way,
     // while at K = 8 (128 bytes per copy and wave) the tiles' 2 KB runs win
     const bool direct = TC_TPACK_DIRECT && next_pow2(tl->K) <= 4 && g->slot_bounds && tl->slot_aligned;
+    // unpack through the tiles, on a group of large tensors, takes the
+    // shorter chunking
+    const tc_chunking& c = unpack && !direct && g->large ? g->tpack_fine : g->tpack;
+    TPackArgs a{g->d_offsets, c.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, c.chunk};
+    const unsigned blocks = static_cast<unsigned>(c.nchunks);
     switch (next_pow2(tl->K)) {
 #define TC_CASE(p) \
     case p: return direct ? run_tpack<p, true>(a, tl->elem, unpack, blocks, stream) \

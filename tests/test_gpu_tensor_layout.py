@@ -112,6 +112,17 @@ def test_pack_tensor_slot_aligned(orc, K, dtype):
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=30 + K, misalign=True)
 
 
+@pytest.mark.parametrize("K", [3, 8, 16])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_pack_tensor_large_tensors_tiled(orc, K, dtype):
+    """A group of large tensors (mean above 32,768 elements) whose tensors
+    start one element into their allocations and whose length is not a
+    multiple of 4: the tiles, the unpack with the group's shorter
+    tensor-layout chunking, across many chunk edges inside each tensor."""
+    sizes = [40001, 33335, 70002, 32769]
+    _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=60 + K, misalign=True)
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_views_and_many_small(orc, dtype):
     _tensor_pack_roundtrip(orc, [1, 2, 3, 5, 8, 13, 4099, 1, 7, 4096, 0, 9001], 4, dtype, seed=5, views=True)
