@@ -79,9 +79,10 @@ int32_t tc_version(void);
  *
  * tc_group_create: sizes is a host array of n >= 1 element counts, each
  * >= 0 (zero-size tensors are allowed); it is copied.  Builds the offset
- * table and the per-chunk segment table used by tc_pack / tc_unpack, and
- * copies both to the current device (synchronously; this is set-up, not
- * part of a step).  Returns NULL on error (n < 1, a negative size, a total
+ * table and, for each way the kernels cut the group into chunks (separate
+ * buffers, tensor-layout pack/unpack, the pipelined step), a table of each
+ * chunk's first tensor, and copies them to the current device
+ * (synchronously; this is set-up, not part of a step).  Returns NULL on error (n < 1, a negative size, a total
  * that overflows int64, allocation failure, no device); see tc_last_error.
  * ---------------------------------------------------------------------- */
 tc_group* tc_group_create(const int64_t* sizes, int32_t n);
