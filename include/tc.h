@@ -82,8 +82,9 @@ int32_t tc_version(void);
  * table and, for each way the kernels cut the group into chunks (separate
  * buffers, tensor-layout pack/unpack, the pipelined step), a table of each
  * chunk's first tensor, and copies them to the current device
- * (synchronously; this is set-up, not part of a step).  Returns NULL on error (n < 1, a negative size, a total
- * that overflows int64, allocation failure, no device); see tc_last_error.
+ * (synchronously; this is set-up, not part of a step).  Returns NULL on
+ * error (n < 1, a negative size, a total that overflows int64, allocation
+ * failure, no device); see tc_last_error.
  * ---------------------------------------------------------------------- */
 tc_group* tc_group_create(const int64_t* sizes, int32_t n);
 
