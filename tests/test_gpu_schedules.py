@@ -207,7 +207,10 @@ def test_period_schedule_matches_oracle(orc, layout):
 
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-@pytest.mark.parametrize("K,N", [(1, 7), (3, 4097), (8, 100003), (16, 5)])
+# (5, 17000003): the separate-buffer kernel's slot path then runs over
+# several windows of source chunks, the last one partial, with copy groups
+# of 4 and 1 and a ragged element tail, for both element sizes.
+@pytest.mark.parametrize("K,N", [(1, 7), (3, 4097), (8, 100003), (16, 5), (5, 17000003)])
 def test_broadcast(orc, layout, dtype, K, N):
     g = tc.Group([N])
     src = torch.randn(N, device=DEV).to(dtype)
