@@ -584,12 +584,12 @@ hipError_t dispatch_easgd(int K, float* const* x, const void* const* g, float* x
 // workgroups resident at one time write about C copies rather than all K,
 // and the later passes over a window find its source in the last-level
 // cache.  The source is read with ordinary (cacheable) loads for that reuse.
-// Measured on MI355X (GB/s; ResNet-50 group, K = 8 / 16 / 4): every copy per
-// workgroup with non-temporal source loads 4,584 / 4,453 / 4,955; the same
-// with cacheable loads 5,690 / 5,240 / 6,365; C = 4 over windows of 8,192
-// chunks (32 MiB of binary32 source) 6,014-6,063 / 5,755-5,793 /
-// 6,340-6,350.  C = 1, 2, 3 and 8, and windows of 2,048 or 32,768 chunks,
-// measured lower.
+// Measured on MI355X with calls rotating over sources that total > 768 MB,
+// so no call finds its source cached by an earlier one (GB/s; ResNet-50
+// group K = 8 / 16 / 4, VGG-16 group K = 8 / 4): every copy per workgroup
+// with non-temporal source loads 4,458-4,490 / 4,912-4,931 / 5,094-5,145 /
+// 5,155-5,200 / 5,198-5,270; C = 4 over windows of 8,192 chunks (32 MiB of
+// binary32 source) 5,297-5,329 / 5,295-5,337 / 5,325-5,354 / 5,627-5,684.
 #ifndef TC_BCAST_COPIES
 #define TC_BCAST_COPIES 4
 #endif
