@@ -53,6 +53,9 @@ WORKLOADS = {
     # unpack are faster on separate buffers, the fused step much faster on the
     # tensor layout, and the whole step slightly faster there
     "many_small_k16_bf16_pipeline": ("many_small_k16_bf16", ("pack", "reduce", "easgd", "unpack"), "tensor"),
+    # the 8-tensor group at K = 2 (7,392 elements): bound by launch and host
+    # overhead, selectable so that a kernel trace can split the two
+    "tiny_k2_pipeline": ("tiny_k2", ("pack", "reduce", "easgd", "unpack"), "tensor"),
 }
 LAYOUTS = ("tensor", "separate")
 
@@ -69,6 +72,18 @@ def op_bytes(op: str, K: int, N: int, s_g: int) -> int:
         return 2 * K * N * 4
     raise ValueError(op)
 
+
+
+def layer_lists(tc, g, flats, sizes):
+    """A model's per-layer tensors for each flat copy: one allocation per
+    layer and copy (torch.empty, no kernel), filled from the flat copies by
+    one tc_unpack launch for all copies.  (A clone per tensor would issue
+    K x n copy kernels: 160,000 for the 10,000-tensor group at K = 16.)"""
+    import torch
+
+    lists = [[torch.empty(s, dtype=f.dtype, device=f.device) for s in sizes] for f in flats]
+    tc.unpack(tc.TensorList(g, lists), flats)
+    return lists
 
 # What defines the kernels measured by the hardware counters: every HIP source
 # and header of the library, and the compiler flags it is built with (the
@@ -199,35 +214,44 @@ def cpu_baseline(wkey: str, ops, sample_elems: int = 30_000_000, min_seconds: fl
            "steps_per_s": round(reps * n / (secs * sum(sizes)), 4),
            "host": host_cpu()}
 
-    # the same oracle functions on every host core: each thread takes a
-    # contiguous block of whole tensors through the four operations (the
-    # operations are elementwise, so the blocks never share an element)
+    # the same oracle functions on every usable host CPU: the flat range is
+    # cut into one contiguous block per thread, inside tensors where a cut
+    # falls there, and each thread takes its block's pieces through the four
+    # operations (the operations are elementwise, so no two threads share an
+    # element and every element is computed as in the single-thread pass)
     from concurrent.futures import ThreadPoolExecutor
 
-    threads = max(1, min(16, out["host"]["usable_cpus"] or 1))
+    threads = max(1, out["host"]["usable_cpus"] or 1)
     offs = np.cumsum([0] + sub)
-    bounds = [int(np.searchsorted(offs, n * j / threads)) for j in range(threads)] + [len(sub)]
-    blocks = [(a, b) for a, b in zip(bounds[:-1], bounds[1:]) if b > a]
+    cuts = [n * j // threads for j in range(threads + 1)]
 
-    def block_pass(a, b):
-        lo, hi = int(offs[a]), int(offs[b])
-        packed = [orc.pack(p[a:b]) for p in g_parts]
+    def pieces(lo, hi):
+        """(tensor, start, stop) of every tensor piece inside [lo, hi)."""
+        t0, t1 = int(np.searchsorted(offs, lo, "right")) - 1, int(np.searchsorted(offs, hi, "left"))
+        return [(t, max(lo, int(offs[t])) - int(offs[t]), min(hi, int(offs[t + 1])) - int(offs[t]))
+                for t in range(t0, t1) if min(hi, int(offs[t + 1])) > max(lo, int(offs[t]))]
+
+    blocks = [(lo, hi, pieces(lo, hi)) for lo, hi in zip(cuts[:-1], cuts[1:]) if hi > lo]
+
+    def block_pass(lo, hi, pcs):
+        packed = [orc.pack([p[t][a:b] for t, a, b in pcs]) for p in g_parts]
         orc.reduce(packed, oracle.AVG)
         xb = [x[lo:hi] for x in x64]
         orc.easgd_step(xb, packed, c64[lo:hi], w.eta, w.rho)
         for x in xb:
-            orc.unpack(x.astype(np.float32), sub[a:b])
+            orc.unpack(x.astype(np.float32), [b - a for _, a, b in pcs])
 
     with ThreadPoolExecutor(max_workers=len(blocks)) as pool:
         preps, t0 = 0, time.perf_counter()
         while preps < max_reps and (preps == 0 or time.perf_counter() - t0 < min_seconds / 2):
-            list(pool.map(lambda ab: block_pass(*ab), blocks))
+            list(pool.map(lambda blk: block_pass(*blk), blocks))
             preps += 1
         psecs = time.perf_counter() - t0
     out["parallel"] = {"value": round(preps * sum(op_bytes(o, w.K, n, s_g) for o in ops) / psecs / 1e9, 3),
                        "unit": "GB/s", "cores": len(blocks), "kind": "oracle",
-                       "sample": f"{preps} passes of the same sample, {len(blocks)} threads, each taking a "
-                                 f"block of whole tensors through {'+'.join(ops)}",
+                       "sample": f"{preps} passes of the same sample, {len(blocks)} threads (every usable CPU), "
+                                 f"each taking one contiguous block of the flat range (cut inside tensors where "
+                                 f"a cut falls there) through {'+'.join(ops)}",
                        "seconds": round(psecs, 3)}
     return out
 
@@ -241,7 +265,7 @@ def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
     dev = "cuda"
     gdt = torch.bfloat16 if w.g_dtype == "bf16" else torch.float32
     print(f"# setup {name} ({layout} layout): n={len(sizes)} N={N} K={K}", file=sys.stderr, flush=True)
-    g_tensors = [wl.separate_tensors(f, sizes) for f in wl.make_gradients(w, N, dev)]
+    g_tensors = layer_lists(tc, g, wl.make_gradients(w, N, dev), sizes)
     g_tl = tc.TensorList(g, g_tensors)
     xs, xc = wl.make_state(w, N, dev)
     gbar = torch.empty(N, dtype=torch.float32, device=dev)
@@ -345,7 +369,7 @@ def run_fused(tc, wl, w, sizes, g, steps, warmup):
     dev = "cuda"
     gdt = torch.bfloat16 if w.g_dtype == "bf16" else torch.float32
     print(f"# setup one-pass pipeline: n={len(sizes)} N={N} K={K}", file=sys.stderr, flush=True)
-    grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in wl.make_gradients(w, N, dev)])
+    grads = tc.TensorList(g, layer_lists(tc, g, wl.make_gradients(w, N, dev), sizes))
     xs, xc = wl.make_state(w, N, dev)
     X = torch.empty(tc.tensor_numel(g, K), dtype=torch.float32, device=dev)
     tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
@@ -405,7 +429,7 @@ def graph_step_rows(tc, wl, reps=200):
     N, K, dev = g.numel, w.K, "cuda"
     gs = wl.make_gradients(w, N, dev)
     xs, xc = wl.make_state(w, N, dev)
-    grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gs])
+    grads = tc.TensorList(g, layer_lists(tc, g, gs, sizes))
     params = tc.TensorList(g, [[torch.empty(n, device=dev) for n in sizes] for _ in range(K)])
     X = torch.zeros(tc.tensor_numel(g, K), device=dev)
     tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
@@ -503,7 +527,7 @@ def config_table(tc, wl, reps=20):
             r["easgd separate"] = row(nb, [lambda: tc.easgd_step(g, xs, gsep[0], xc, w.eta, w.rho)])
             r["easgd tensor"] = row(nb, [lambda: tc.easgd_step_tensor(g, K, X, gten[0], xc2, w.eta, w.rho)])
             if "pack" in w.ops:
-                grads = tc.TensorList(g, [wl.separate_tensors(f, sizes) for f in gsep[0]])
+                grads = tc.TensorList(g, layer_lists(tc, g, gsep[0], sizes))
                 params = tc.TensorList(g, [[torch.empty(n, device=dev) for n in sizes] for _ in range(K)])
                 r["pipeline (easgd_pipeline_tensor)"] = row(
                     fused_bytes(K, N, s_g), [lambda: tc.easgd_pipeline_tensor(grads, params, gten[0], avg, X, xc2,

@@ -148,14 +148,18 @@ int32_t tc_unpack(const tc_tensorlist* tl, const void* const* flat, void* stream
  * pairwise tree (adjacent pairs, level by level; an odd last term is carried
  * up), and AVG divides the sum by K with one correctly rounded division; so
  * the AVG of K identical copies returns the copy exactly for power-of-two K.
- * out may be identical to one of the inputs (in place); partial overlaps are
- * undefined.  K in [1, TC_MAX_K].
+ * out may be identical to one of the inputs (in place); a partial overlap
+ * returns TC_EINVAL.  K in [1, TC_MAX_K].
  * ---------------------------------------------------------------------- */
 int32_t tc_reduce(const tc_group* g, int32_t K, const float* const* in,
                   float* out, int32_t op, void* stream);
 
 /* As tc_reduce, with inputs of type in_dtype (TC_F32 or TC_BF16); the sum
- * is accumulated and returned in binary32. */
+ * is accumulated and returned in binary32.  In place is allowed for TC_F32
+ * inputs only: a binary32 output element is twice as wide as a bfloat16
+ * input element, so an output written over a bfloat16 input would overwrite
+ * input elements that other lanes have not yet read.  With TC_BF16 inputs,
+ * an out that overlaps any input returns TC_EINVAL. */
 int32_t tc_reduce_ex(const tc_group* g, int32_t K, const void* const* in,
                      int32_t in_dtype, float* out, int32_t op, void* stream);
 

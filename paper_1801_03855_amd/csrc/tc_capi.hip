@@ -239,9 +239,12 @@ TC_API int32_t tc_reduce_ex(const tc_group* g, int32_t K, const void* const* in,
         if (!in[i]) { set_error("in[%d] is NULL", i); return TC_EINVAL; }
         if (!aligned(in[i], es)) { set_error("in[%d] is not element-aligned", i); return TC_EINVAL; }
         vec = vec && aligned(in[i], es == 4 ? 16 : 8);
-        // in place is allowed only as exact identity with an input
-        if (in[i] != out && overlap(in[i], g->N * es, out, g->N * 4)) {
-            set_error("out partially overlaps in[%d]", i);
+        // in place is allowed only as exact identity with a binary32 input:
+        // a binary32 output slot covers two bfloat16 input slots, which
+        // other lanes read
+        if (overlap(in[i], g->N * es, out, g->N * 4) && (in[i] != out || in_dtype != TC_F32)) {
+            set_error(in_dtype == TC_F32 ? "out partially overlaps in[%d]"
+                                         : "out overlaps in[%d] (no in-place reduction of bfloat16 inputs)", i);
             return TC_EINVAL;
         }
     }

@@ -523,6 +523,19 @@ def test_argument_errors():
     assert L.tc_reduce(g.handle, 3, pa, None, 0, s) == tc.TC_EINVAL
     assert L.tc_reduce(g.handle, 3, pa, a[1].data_ptr() + 4, 0, s) == tc.TC_EINVAL  # partial overlap
     assert "overlap" in tc.last_error()
+    # bfloat16 inputs: out may not overlap an input at all, not even as the
+    # same pointer (a binary32 output slot covers two input slots)
+    big = torch.zeros(256, dtype=torch.bfloat16, device=DEV)
+    h = [big[0:32], big[64:96]]
+    hp = _ptr_array([t.data_ptr() for t in h])
+    wide = torch.zeros(32, device=DEV)
+    g32 = tc.Group([32])
+    assert L.tc_reduce_ex(g32.handle, 2, hp, tc.TC_BF16, h[0].data_ptr(), 0, s) == tc.TC_EINVAL
+    assert "bfloat16" in tc.last_error()
+    assert L.tc_reduce_ex(g32.handle, 2, hp, tc.TC_BF16, big[80:].data_ptr(), 0, s) == tc.TC_EINVAL
+    assert L.tc_reduce_ex(g32.handle, 2, hp, tc.TC_BF16, wide.data_ptr(), 0, s) == tc.TC_OK
+    fp = _ptr_array([wide.data_ptr(), a[0].data_ptr()])
+    assert L.tc_reduce_ex(tc.Group([16]).handle, 2, fp, tc.TC_F32, wide.data_ptr(), 0, s) == tc.TC_OK
     xc = torch.zeros(16, device=DEV)
     xp = _ptr_array([t.data_ptr() for t in a])
     gp = _ptr_array([t.data_ptr() for t in [out, out, out]])

@@ -9,7 +9,8 @@ import torch
 
 import paper_1801_03855_amd as tc
 from paper_1801_03855_amd import workloads as wl
-from tests.helpers import TOL, assert_bits_equal, assert_close, assert_exact, host_f32, host_stored, widened
+from tests.helpers import (TOL, assert_bits_equal, assert_close, assert_exact, easgd_mags, host_f32, host_stored,
+                           widened)
 
 pytestmark = pytest.mark.gpu
 
@@ -194,15 +195,24 @@ def test_period_schedule_matches_oracle(orc, layout):
     torch.cuda.synchronize()
     rx = [a.astype(np.float64) for a in h_x]
     rc = h_c.astype(np.float64)
-    span = np.maximum.reduce([np.abs(a.astype(np.float64)) for a in h_x] + [np.abs(rc)]) + 0.1
+    # guard: each step's own magnitudes (elastic step: easgd_mags; SGD step:
+    # |x_i| + eta |g_i|, the center untouched), taken at the largest value
+    # each element reaches along the oracle's trajectory
+    mx = [np.zeros_like(a) for a in rx]
+    mc = np.zeros_like(rc)
     for t in range(10):
         if t % tau == 0:
+            sx, sc = easgd_mags(rx, h_g, rc, w.eta, w.rho)
             orc.easgd_step(rx, h_g, rc, w.eta, w.rho)
         else:
+            sx = [np.abs(a) + w.eta * np.abs(widened(b)) for a, b in zip(rx, h_g)]
+            sc = np.abs(rc)
             orc.sgd_step(rx, h_g, w.eta)
+        mx = [np.maximum(a, b) for a, b in zip(mx, sx)]
+        mc = np.maximum(mc, sc)
     for i, got in enumerate(L.x_host()):
-        assert_close(got, rx[i], span, f"{layout} x[{i}]")
-    assert_close(host_f32(xc), rc, span, f"{layout} x_c")
+        assert_close(got, rx[i], mx[i], f"{layout} x[{i}]")
+    assert_close(host_f32(xc), rc, mc, f"{layout} x_c")
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
