@@ -159,7 +159,8 @@ template <int P, int U, typename I>
 __device__ __forceinline__ I first_slot() {
     constexpr int SPW = 64 / P;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    return static_cast<I>(blockIdx.x) * (4 * U * SPW) + static_cast<I>(wave * U * SPW + lane / P);
+    const uint32_t b = tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x);
+    return static_cast<I>(b) * (4 * U * SPW) + static_cast<I>(wave * U * SPW + lane / P);
 }
 
 // ------------------------------------------------------------- reduce
