@@ -57,8 +57,12 @@ def test_counter_summaries_are_tied_to_the_compiler_flags(monkeypatch):
 
 def test_recorded_traffic_matches_algorithmic_bytes_when_current():
     """A committed FETCH_SIZE/WRITE_SIZE summary taken from the current
-    sources reports HBM traffic within 0.5% of the algorithmic bytes (no
-    re-reads, no wasted writes); a stale one is ignored."""
+    sources reports HBM traffic within 0.5% of the algorithmic bytes on
+    groups whose tensors are all slot-aligned (no re-reads, no wasted
+    writes); on the 10,000-tensor group, whose tensors mostly start and end
+    inside 16-byte granules, the reductions and the separate-buffer step stay
+    within 0.5% and no kernel exceeds 6% (whole granules read at misaligned
+    edges); a stale summary is ignored."""
     for wname, (wkey, ops, layout) in bench.WORKLOADS.items():
         for lay in ("tensor", "separate"):
             rec = bench.recorded_traffic(wname, lay)
@@ -67,10 +71,13 @@ def test_recorded_traffic_matches_algorithmic_bytes_when_current():
             w = wl.WORKLOADS[wkey]
             n = sum(w.sizes())
             s_g = 2 if w.g_dtype == "bf16" else 4
+            misaligned = any(s % 4 for s in w.sizes()[:-1])
             for op, traffic in rec.items():
                 alg = (bench.fused_bytes(w.K, n, s_g, op == "pipeline") if op.startswith("pipeline")
                        else bench.op_bytes(op, w.K, n, s_g))
-                assert abs(traffic / alg - 1) < 5e-3, (wname, lay, op, traffic, alg)
+                exact = not misaligned or op == "reduce" or (op == "easgd" and lay == "separate")
+                assert traffic >= alg * (1 - 5e-3), (wname, lay, op, traffic, alg)
+                assert traffic / alg - 1 < (5e-3 if exact else 0.06), (wname, lay, op, traffic, alg)
 
 
 def test_source_hash_ignores_comments_only(tmp_path, monkeypatch):
