@@ -482,6 +482,56 @@ __device__ __forceinline__ void store_bytes(uintptr_t D, u4 v) {
     else gst_nt<u2>(D, u2{v.x, v.y});
 }
 
+// Lane l + 1's value in lane l, within a row of 16 lanes (DPP row_shl:1);
+// the last lane of a row gets 0.
+__device__ __forceinline__ uint32_t from_next_lane(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x101, 0xF, 0xF, true));
+}
+
+// Gather of 16-byte windows that consecutive lanes take from consecutive
+// addresses (a run of one copy's slots).  A window at an address that is not
+// a multiple of 16 spans two aligned granules, the second of which is the
+// first granule of the next lane's window.  Each lane loads the granule
+// holding its window's start for every window before anything else; it then
+// takes the second granule from lane l + 1 when that lane loaded exactly
+// that granule (checked on the addresses) and loads it itself otherwise (a
+// run's or a row's last lane, the next lane in another run).  N windows per
+// lane; window q is skipped when S[q] == 0.  All lanes of the wave must take
+// part (the exchange is a cross-lane move).  Measured on MI355X in the
+// binary32 tiled pack, with every piece's address found before the first
+// load: ResNet-50 at K = 8 6.3-7.1% faster than a search and a load per
+// piece in turn.  For 8-byte slots (bfloat16) the same exchange was 3.5%
+// slower than two loads per misaligned window; there the addresses-first
+// order alone gained 5.6% (10,000 tensors, K = 16).
+template <int N>
+__device__ __forceinline__ void load_windows(const uintptr_t (&S)[N], u4 (&out)[N]) {
+    u4 g0[N], g1[N];
+    bool next[N];
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+        g0[q] = u4{0u, 0u, 0u, 0u};
+        if (S[q]) g0[q] = gld_nt<u4>(S[q] & ~uintptr_t(15));
+    }
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+        const uintptr_t g = S[q] & ~uintptr_t(15);
+        const uint64_t n = static_cast<uint64_t>(from_next_lane(static_cast<uint32_t>(g))) |
+                           (static_cast<uint64_t>(from_next_lane(static_cast<uint32_t>(static_cast<uint64_t>(g) >> 32)))
+                            << 32);
+        next[q] = S[q] && (S[q] & 15) && n == static_cast<uint64_t>(g) + 16;
+        g1[q] = u4{0u, 0u, 0u, 0u};
+        if (S[q] && (S[q] & 15) && !next[q]) g1[q] = gld_nt<u4>(g + 16);
+    }
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+        const u4 n4 = u4{from_next_lane(g0[q].x), from_next_lane(g0[q].y), from_next_lane(g0[q].z),
+                         from_next_lane(g0[q].w)};
+        if (next[q]) g1[q] = n4;
+        const uint32_t sh = static_cast<uint32_t>(S[q] & 15);
+        out[q] = sh ? funnel(g0[q], g1[q], sh) : g0[q];
+    }
+}
+
 // Workgroup b moves chunk b of all K copies through LDS, M slots at a time
 // (M = 1024/P, at least 16: a 16 KB tile for binary32), so that both global
 // sides are contiguous:
@@ -515,9 +565,20 @@ __device__ __forceinline__ void store_bytes(uintptr_t D, u4 v) {
 #ifndef TC_TPACK_DIRECT
 #define TC_TPACK_DIRECT 1
 #endif
+// The direct binary32 pack and unpack are compiled for at least 4 waves per
+// SIMD (amdgpu_waves_per_eu; they already run at 6, so the hint takes no
+// occupancy): measured on MI355X, VGG-16 at K = 4 packs 3% and unpacks 2%
+// faster, ResNet-50 at K = 4 4% and 3.5%, whatever the hint's value (4, 5
+// or 6).  The same hint on the tiled kernels, the steps and the pipelined
+// step measured level or up to 9% slower.
+#ifndef TC_TPACK_WAVES_DIRECT
+#define TC_TPACK_WAVES_DIRECT 4
+#endif
 
 template <int P, typename T, bool UNPACK, bool DIRECT>
-__global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256),
+                          amdgpu_waves_per_eu(DIRECT && sizeof(T) == 4 ? TC_TPACK_WAVES_DIRECT : 1)))
+void tensor_pack_kernel(TPackArgs a) {
     constexpr int ES = sizeof(T);
     constexpr int SB = 4 * ES;                      // slot bytes
     constexpr int TILE = UNPACK && ES == 4 && P >= 16 ? TC_TUNPACK_TILE_WIDE : TC_TPACK_TILE;
@@ -617,14 +678,29 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                 return v;
             };
             if constexpr (SB == 16) {
+                // the addresses of every piece first (the segment searches in
+                // LDS), then the loads through load_windows; a slot spanning
+                // tensors element by element
                 u4 v[R];
                 bool ok[R];
+                uintptr_t S[R];
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int q = threadIdx.x + r * 256;
                     const int kk = q / M, jl = q % M;
                     ok[r] = kk < K && jl < mt;
-                    if (ok[r]) v[r] = slot_piece(kk, t0 + jl);
+                    S[r] = 0;
+                    if (ok[r]) {
+                        const int jr = 4 * (t0 + jl);
+                        const int sg = find(jr);
+                        if (jr + 4 <= rel(sg + 1)) S[r] = base(kk, sg) + static_cast<uintptr_t>(jr) * ES;
+                    }
+                }
+                load_windows<R>(S, v);
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    if (ok[r] && !S[r]) v[r] = slot_piece(q / M, t0 + q % M);
                 }
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
@@ -632,24 +708,35 @@ __global__ __launch_bounds__(256) void tensor_pack_kernel(TPackArgs a) {
                     if (ok[r]) *reinterpret_cast<u4*>(tile(q % M, q / M)) = v[r];
                 }
             } else {
-                // 8-byte slots: a lane takes two consecutive slots of one copy,
-                // 16 source bytes read as one (funnel-shifted) granule pair
-                // when both lie in one tensor
+                // 8-byte slots: a lane takes two consecutive slots of one
+                // copy, 16 source bytes read as one (funnel-shifted) granule
+                // pair when both lie in one tensor; addresses first, then the
+                // loads, as above
                 constexpr int R2 = R / 2, MH = M / 2;
                 u4 v[R2];
                 bool ok0[R2], ok1[R2];
+                uintptr_t S[R2];
 #pragma unroll
                 for (int r = 0; r < R2; ++r) {
                     const int q = threadIdx.x + r * 256;
                     const int kk = q / MH, jl = 2 * (q % MH);
                     ok0[r] = kk < K && jl < mt;
                     ok1[r] = kk < K && jl + 1 < mt;
-                    if (!ok0[r]) continue;
-                    const int jr = 4 * (t0 + jl);
-                    const int s = find(jr);
-                    if (ok1[r] && jr + 8 <= rel(s + 1)) {
-                        v[r] = load_bytes<16>(base(kk, s) + static_cast<uintptr_t>(jr) * ES);
-                    } else {
+                    S[r] = 0;
+                    if (ok1[r]) {
+                        const int jr = 4 * (t0 + jl);
+                        const int sg = find(jr);
+                        if (jr + 8 <= rel(sg + 1)) S[r] = base(kk, sg) + static_cast<uintptr_t>(jr) * ES;
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < R2; ++r)
+                    if (S[r]) v[r] = load_bytes<16>(S[r]);
+#pragma unroll
+                for (int r = 0; r < R2; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    const int kk = q / MH, jl = 2 * (q % MH);
+                    if (ok0[r] && !S[r]) {
                         const u4 a0 = slot_piece(kk, t0 + jl);
                         const u4 a1 = ok1[r] ? slot_piece(kk, t0 + jl + 1) : u4{0u, 0u, 0u, 0u};
                         v[r] = u4{a0.x, a0.y, a1.x, a1.y};
@@ -970,14 +1057,27 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
                 return v;
             };
             if constexpr (SB == 16) {
+                // as in tc_pack_tensor: addresses first, then load_windows
                 u4 v[R];
                 bool ok[R];
+                uintptr_t S[R];
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     const int q = threadIdx.x + r * 256;
                     const int kk = q / M, jl = q % M;
                     ok[r] = kk < K && jl < mt;
-                    if (ok[r]) v[r] = slot_piece(kk, t0 + jl);
+                    S[r] = 0;
+                    if (ok[r]) {
+                        const int jr = 4 * (t0 + jl);
+                        const int sg = find(jr);
+                        if (jr + 4 <= rel(sg + 1)) S[r] = gbase(kk, sg) + static_cast<uintptr_t>(jr) * ES;
+                    }
+                }
+                load_windows<R>(S, v);
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    if (ok[r] && !S[r]) v[r] = slot_piece(q / M, t0 + q % M);
                 }
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
@@ -985,23 +1085,33 @@ __global__ __launch_bounds__(256) void tensor_pipeline_kernel(TPipeArgs a) {
                     if (ok[r]) *reinterpret_cast<u4*>(gtile(q % M, q / M)) = v[r];
                 }
             } else {
-                // 8-byte slots: two consecutive slots of one copy per lane, as
-                // in tc_pack_tensor
+                // 8-byte slots: two consecutive slots of one copy per lane,
+                // as in tc_pack_tensor
                 constexpr int R2 = R / 2, MH = M / 2;
                 u4 v[R2];
                 bool ok0[R2], ok1[R2];
+                uintptr_t S[R2];
 #pragma unroll
                 for (int r = 0; r < R2; ++r) {
                     const int q = threadIdx.x + r * 256;
                     const int kk = q / MH, jl = 2 * (q % MH);
                     ok0[r] = kk < K && jl < mt;
                     ok1[r] = kk < K && jl + 1 < mt;
-                    if (!ok0[r]) continue;
-                    const int jr = 4 * (t0 + jl);
-                    const int s = find(jr);
-                    if (ok1[r] && jr + 8 <= rel(s + 1)) {
-                        v[r] = load_bytes<16>(gbase(kk, s) + static_cast<uintptr_t>(jr) * ES);
-                    } else {
+                    S[r] = 0;
+                    if (ok1[r]) {
+                        const int jr = 4 * (t0 + jl);
+                        const int sg = find(jr);
+                        if (jr + 8 <= rel(sg + 1)) S[r] = gbase(kk, sg) + static_cast<uintptr_t>(jr) * ES;
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < R2; ++r)
+                    if (S[r]) v[r] = load_bytes<16>(S[r]);
+#pragma unroll
+                for (int r = 0; r < R2; ++r) {
+                    const int q = threadIdx.x + r * 256;
+                    const int kk = q / MH, jl = 2 * (q % MH);
+                    if (ok0[r] && !S[r]) {
                         const u4 a0 = slot_piece(kk, t0 + jl);
                         const u4 a1 = ok1[r] ? slot_piece(kk, t0 + jl + 1) : u4{0u, 0u, 0u, 0u};
                         v[r] = u4{a0.x, a0.y, a1.x, a1.y};
