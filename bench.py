@@ -415,6 +415,45 @@ def _time_launches(fns, reps):
     return t[reps // 2], t[0]
 
 
+def tensorlist_rows(tc, wl, reps=5):
+    """Host cost of describing K per-layer tensor lists to the library
+    (tc_tensorlist_create: argument checks, a hipMalloc of the K*n-pointer
+    table and a synchronous upload), which a caller whose per-layer tensors
+    move between steps would pay once per step: the raw C call on a
+    prepared pointer array, median of reps, and the matching destroy."""
+    import ctypes
+
+    import torch
+
+    out = {}
+    L = tc.lib()
+    for wkey in ("resnet50_k8_easgd", "many_small_k16_bf16"):
+        w = wl.WORKLOADS[wkey]
+        sizes = w.sizes()
+        g = tc.Group(sizes)
+        dt = torch.bfloat16 if w.g_dtype == "bf16" else torch.float32
+        flats = [torch.empty(g.numel, dtype=dt, device="cuda") for _ in range(w.K)]
+        lists = [wl.split_views(f, sizes) for f in flats]
+        ptrs = tc._ptr_array([t.data_ptr() if t.numel() else 0 for c in lists for t in c])
+        code = tc.TC_BF16 if dt == torch.bfloat16 else tc.TC_F32
+        times = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            h = L.tc_tensorlist_create(g.handle, w.K, ptrs, code)
+            t1 = time.perf_counter()
+            if not h:
+                raise RuntimeError(tc.last_error())
+            L.tc_tensorlist_destroy(h)
+            times.append(t1 - t0)
+        times.sort()
+        out[wkey] = {"pointers": w.K * len(sizes), "create_ms_median": round(times[reps // 2] * 1e3, 4),
+                     "create_ms_min": round(times[0] * 1e3, 4)}
+        del flats, lists
+    torch.cuda.empty_cache()
+    return out
+
+
 def graph_step_rows(tc, wl, reps=200):
     """The tiny group's whole step (pack, AVG, fused step, unpack on the
     tensor layout; and the same as one easgd_pipeline_tensor launch), timed
@@ -710,6 +749,7 @@ def main():
     if not args.no_configs:
         configs = config_table(tc, wl)
         configs["tiny_k2"]["whole step, eager and HIP graph"] = graph_step_rows(tc, wl)
+        configs["tensor_list_create"] = tensorlist_rows(tc, wl)
 
     extra = None
     if not args.no_next_rows and args.workload == "resnet50_k8_pipeline":

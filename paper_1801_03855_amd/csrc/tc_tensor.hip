@@ -22,6 +22,10 @@
 
 #include "tc_internal.h"
 
+#ifndef TC_TEASGD_CSHARE
+#define TC_TEASGD_CSHARE 1
+#endif
+
 namespace tc {
 namespace {
 
@@ -250,33 +254,65 @@ struct TEasgdArgs {
     int K;
 };
 
+// A wave of the step covers WS = U * 64 / P consecutive slots.  At P >= 16
+// that is at most 8 slots, 128 bytes of the center, which U instructions of
+// 64 / P slots each would read and write in pieces of 16 to 64 bytes; the
+// center is then read by one instruction (lane m < WS takes slot m of the
+// wave) and handed to the slot groups with cross-lane reads, and the new
+// center gathered back into lanes 0 .. WS - 1 for one store.
+__device__ __forceinline__ f4 shfl4(f4 v, int src) {
+    return f4{__shfl(v.x, src, 64), __shfl(v.y, src, 64), __shfl(v.z, src, 64), __shfl(v.w, src, 64)};
+}
+
 template <int P, typename T, int U, typename I>
 __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
     constexpr int SPW = 64 / P;
+    constexpr int WS = U * SPW;
+    constexpr bool kShare = P >= 16 && TC_TEASGD_CSHARE;
     const int K = a.K;
     const int i = threadIdx.x % P;
+    const int lane = threadIdx.x & 63;
     const I j0 = first_slot<P, U, I>();
+    const I jw = j0 - static_cast<I>(lane / P);  // the wave's first slot
     const I nslot = static_cast<I>(a.nslot);
     f4 x[U], g[U], c[U];
+    if constexpr (kShare) {
+        const I jm = jw + static_cast<I>(lane % WS);
+        const f4 cw = jm < nslot ? load_slot(a.xc, jm) : f4(0.0f);
+#pragma unroll
+        for (int u = 0; u < U; ++u) c[u] = shfl4(cw, lane / P + u * SPW);
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const I j = j0 + I(u) * SPW;
         const bool slot = j < nslot;
-        c[u] = slot ? load_slot(a.xc, j) : f4(0.0f);
+        if constexpr (!kShare) c[u] = slot ? load_slot(a.xc, j) : f4(0.0f);
         const bool live = slot && i < K;
         x[u] = live ? load_slot(a.x, j * I(K) + I(i)) : f4(0.0f);
         g[u] = live ? load_slot(a.g, j * I(K) + I(i)) : f4(0.0f);
     }
     const f4 rho = f4(a.rho), neg_eta = f4(-a.eta), alpha = f4(a.a);
+    f4 cn[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const I j = j0 + I(u) * SPW;
         const bool live = j < nslot && i < K;
         const f4 d = live ? x[u] - c[u] : f4(0.0f);
         const f4 xn = fma4(neg_eta, fma4(rho, d, g[u]), x[u]);
-        const f4 cn = fma4(alpha, group_sum4<P>(d), c[u]);
+        cn[u] = fma4(alpha, group_sum4<P>(d), c[u]);
         if (live) store_slot(a.x, j * I(K) + I(i), xn);
-        if (j < nslot && i == 0) store_slot(a.xc, j, cn);
+        if (!kShare && j < nslot && i == 0) store_slot(a.xc, j, cn[u]);
+    }
+    if constexpr (kShare) {
+        // lane m < WS stores slot jw + m, whose new center slot group m % SPW
+        // computed in pass m / SPW
+        f4 out = f4(0.0f);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const f4 t = shfl4(cn[u], (lane % SPW) * P);
+            if (lane / SPW == u) out = t;
+        }
+        if (lane < WS && jw + static_cast<I>(lane) < nslot) store_slot(a.xc, jw + static_cast<I>(lane), out);
     }
     if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot
         const int64_t e = 4 * a.nslot + threadIdx.x;
