@@ -612,14 +612,26 @@ __device__ __forceinline__ void load_windows(const uintptr_t (&S)[N], u4 (&out)[
 #define TC_TPACK_WAVES_DIRECT 4
 #endif
 
+// Slots per LDS tile: the tile's pieces over P, at least 16, and no more
+// than the slots of a chunk (TC_TPACK_CHUNK / 4; tiles larger than the chunk
+// leave lanes idle), but at least one piece per lane (two for the bfloat16
+// pack, whose lanes take two slots), which at P <= 2 sets the size.
+template <int P, int ES, bool UNPACK>
+constexpr int tpack_tile_slots() {
+    constexpr int TILE = UNPACK && ES == 4 && P >= 16 ? TC_TUNPACK_TILE_WIDE : TC_TPACK_TILE;
+    constexpr int MT = TILE / P > 16 ? TILE / P : 16;
+    constexpr int CS = TC_TPACK_CHUNK / 4;
+    constexpr int MIN = (ES == 2 && !UNPACK ? 512 : 256) / P;
+    return MT <= CS ? MT : (MIN > CS ? MIN : CS);
+}
+
 template <int P, typename T, bool UNPACK, bool DIRECT>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256),
                           amdgpu_waves_per_eu(DIRECT && sizeof(T) == 4 ? TC_TPACK_WAVES_DIRECT : 1)))
 void tensor_pack_kernel(TPackArgs a) {
     constexpr int ES = sizeof(T);
     constexpr int SB = 4 * ES;                      // slot bytes
-    constexpr int TILE = UNPACK && ES == 4 && P >= 16 ? TC_TUNPACK_TILE_WIDE : TC_TPACK_TILE;
-    constexpr int M = TILE / P > 16 ? TILE / P : 16;  // slots per LDS tile
+    constexpr int M = tpack_tile_slots<P, ES, UNPACK>();  // slots per LDS tile
     constexpr int ROW = (P + 1) * SB;               // padded tile row, bytes
     __shared__ int32_t s_rel[kMaxStage + 1];
     __shared__ uintptr_t s_base[kMaxStage];
@@ -698,7 +710,7 @@ void tensor_pack_kernel(TPackArgs a) {
         // each phase moves M*P = 1024 pieces: 4 per lane, all loads issued
         // before the first write
         constexpr int R = (M * P) / 256;
-        if (!UNPACK) {
+        if constexpr (!UNPACK) {
             // copies -> tile: lanes walk consecutive slots of one copy
             auto slot_piece = [&](int kk, int js) -> u4 {  // one slot of copy kk
                 const int jr = 4 * js;
@@ -1380,9 +1392,26 @@ hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, floa
 }
 
 template <int P, bool DIRECT>
-hipError_t run_tpack(const TPackArgs& a, int elem, bool unpack, unsigned blocks, hipStream_t stream) {
-    dim3 grid(blocks);
-    if (elem == 2) {
+hipError_t run_tpack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStream_t stream) {
+    const tc_group* g = tl->g;
+    // Chunks:
+    // - at P <= 2 a chunk of TC_TPACK_CHUNK elements moves little (4-16 KB),
+    //   so these lists take the longer chunks of the separate-buffer pack
+    //   (2,048 or 4,096 elements; measured on MI355X, K = 1 and 2 on
+    //   ResNet-50, VGG-16 and 10,000 small tensors: pack 2-80% faster,
+    //   unpack 12-57% in bfloat16 and 20-35% for misaligned lists), except
+    //   the direct binary32 unpack at P = 2 (1-3% slower with them);
+    // - unpack through the tiles, on a group of large tensors, takes the
+    //   shorter chunking when a tile fits in its chunks (P >= 8; at P = 4
+    //   the tiles would leave half the lanes idle).
+    constexpr int fine_slots = TC_TPACK_CHUNK_FINE / 4;
+    const bool fits = tl->elem == 2 ? tpack_tile_slots<P, 2, true>() <= fine_slots
+                                    : tpack_tile_slots<P, 4, true>() <= fine_slots;
+    const bool longer = P <= 2 && !(DIRECT && unpack && tl->elem == 4 && P == 2);
+    const tc_chunking& c = longer ? g->sep : unpack && !DIRECT && g->large && fits ? g->tpack_fine : g->tpack;
+    TPackArgs a{g->d_offsets, c.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, c.chunk};
+    dim3 grid(static_cast<unsigned>(c.nchunks));
+    if (tl->elem == 2) {
         if (unpack) hipLaunchKernelGGL((tensor_pack_kernel<P, uint16_t, true, DIRECT>), grid, dim3(256), 0, stream, a);
         else hipLaunchKernelGGL((tensor_pack_kernel<P, uint16_t, false, DIRECT>), grid, dim3(256), 0, stream, a);
     } else {
@@ -1397,18 +1426,17 @@ hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack
     // straight through registers when every tensor boundary before the last,
     // partial slot falls on a slot boundary, every tensor of the list is
     // slot-aligned and a wave still moves >= 256 contiguous bytes of each copy
-    // (P <= 4): measured on MI355X, VGG-16 at K = 4 packs 5% faster that way,
-    // while at K = 8 (128 bytes per copy and wave) the tiles' 2 KB runs win
-    const bool direct = TC_TPACK_DIRECT && next_pow2(tl->K) <= 4 && g->slot_bounds && tl->slot_aligned;
-    // unpack through the tiles, on a group of large tensors, takes the
-    // shorter chunking
-    const tc_chunking& c = unpack && !direct && g->large ? g->tpack_fine : g->tpack;
-    TPackArgs a{g->d_offsets, c.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, c.chunk};
-    const unsigned blocks = static_cast<unsigned>(c.nchunks);
+    // ((64 / P) slots of 4 * elem bytes: P <= 4 for binary32, P <= 2 for
+    // bfloat16).  Measured on MI355X: VGG-16 at K = 4 packs 5% faster that way
+    // in binary32, while at K = 8 (128 bytes per copy and wave) the tiles' 2 KB
+    // runs win; in bfloat16 the tiles win at K = 4 (128 bytes per copy and
+    // wave; VGG-16 +15%, ResNet-50 +17%) and lose at K = 2 (up to 19%).
+    const bool direct = TC_TPACK_DIRECT && (64 / next_pow2(tl->K)) * 4 * tl->elem >= 256 && g->slot_bounds &&
+                        tl->slot_aligned;
     switch (next_pow2(tl->K)) {
 #define TC_CASE(p) \
-    case p: return direct ? run_tpack<p, true>(a, tl->elem, unpack, blocks, stream) \
-                          : run_tpack<p, false>(a, tl->elem, unpack, blocks, stream);
+    case p: return direct ? run_tpack<p, true>(tl, tensor, unpack, stream) \
+                          : run_tpack<p, false>(tl, tensor, unpack, stream);
         TC_FOR_P(TC_CASE)
 #undef TC_CASE
         default: return hipErrorInvalidValue;

@@ -100,7 +100,7 @@ def test_pack_tensor_ragged_and_misaligned(orc, K, dtype):
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=K, misalign=True)
 
 
-@pytest.mark.parametrize("K", [1, 3, 8, 16, 64])
+@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 16, 64])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_slot_aligned(orc, K, dtype):
     """Slot-multiple tensor lengths before a ragged last tensor, tensors in
@@ -112,21 +112,34 @@ def test_pack_tensor_slot_aligned(orc, K, dtype):
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=30 + K, misalign=True)
 
 
-@pytest.mark.parametrize("K", [3, 8, 16])
+@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 16])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_large_tensors_tiled(orc, K, dtype):
     """A group of large tensors (mean above 32,768 elements) whose tensors
     start one element into their allocations and whose length is not a
-    multiple of 4: the tiles, the unpack with the group's shorter
-    tensor-layout chunking, across many chunk edges inside each tensor."""
+    multiple of 4: the tiles, across many chunk edges inside each tensor,
+    in each chunking the kernels pick (the longer separate-buffer chunks at
+    K <= 2, the unpack's shorter tensor-layout chunks at K >= 8)."""
     sizes = [40001, 33335, 70002, 32769]
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=60 + K, misalign=True)
+
+
+@pytest.mark.parametrize("K", [1, 2, 3, 4])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_pack_tensor_large_tensors_slot_aligned(orc, K, dtype):
+    """Large slot-multiple tensors in their own allocations, ragged last
+    tensor: straight through registers where a wave moves at least 256
+    bytes of each copy (binary32 up to K = 4, bfloat16 up to K = 2), through
+    the tiles otherwise (bfloat16 at K = 3, 4)."""
+    sizes = [40000, 33336, 70004, 32768, 5]
+    _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=70 + K)
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_views_and_many_small(orc, dtype):
     _tensor_pack_roundtrip(orc, [1, 2, 3, 5, 8, 13, 4099, 1, 7, 4096, 0, 9001], 4, dtype, seed=5, views=True)
     _tensor_pack_roundtrip(orc, wl.many_small_sizes(1500, seed=9), 16, dtype, seed=6, misalign=True)
+    _tensor_pack_roundtrip(orc, wl.many_small_sizes(1500, seed=9), 2, dtype, seed=8, misalign=True)
     rng = np.random.default_rng(4)
     # tensors of 0 or 1 elements: about 2,000 per 1,024-element chunk, more than
     # the LDS tables hold, so the global-table search runs too
