@@ -172,11 +172,12 @@ def test_k_and_ragged_tail(orc, K):
     _run(orc, sizes, K, seed=K)
 
 
-@pytest.mark.parametrize("K,gdt", [(3, torch.float32), (8, torch.float32), (16, torch.bfloat16), (5, torch.bfloat16)])
+@pytest.mark.parametrize("K,gdt", [(1, torch.float32), (2, torch.float32), (2, torch.bfloat16), (3, torch.float32),
+                                   (8, torch.float32), (16, torch.bfloat16), (5, torch.bfloat16)])
 def test_misaligned_tensors(orc, K, gdt):
     """Every per-layer tensor one element into its allocation: the gather
-    funnel-shifts, the scatter writes whole granules inside runs, with tile
-    edges as run ends."""
+    reads unaligned windows, the scatter writes whole granules inside runs,
+    with tile edges as run ends (K <= 2: the longer chunks)."""
     sizes = [513, 4099, 6, 70001, 3, 1030]
     _run(orc, sizes, K, gdt=gdt, seed=10 + K, misalign=True)
 
@@ -216,6 +217,7 @@ def test_many_tensors_per_chunk(orc):
     rng = np.random.default_rng(9)
     sizes = [int(s) for s in rng.integers(0, 2, 6000)]
     _run(orc, sizes, 4, gdt=torch.bfloat16, seed=9, misalign=True)
+    _run(orc, sizes, 2, gdt=torch.bfloat16, seed=29, misalign=True)
     _run(orc, sizes, 16, seed=19)
 
 
