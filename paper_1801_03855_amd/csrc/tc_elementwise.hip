@@ -16,7 +16,12 @@
 //
 // The K terms are summed by a pairwise tree (adjacent pairs, level by level,
 // an odd last term carried up) fully unrolled for K <= 16; larger K is
-// summed as trees of 16 (zero-padded) combined by a tree of the partials.
+// summed as trees of 16 (zero-padded) combined by a tree of the four
+// partials (zero-padded).  The kernels for K > 16 loop over the groups of 16
+// copies without unrolling, so that only one group's pointers are live: fully
+// unrolled over 64 copies they held 128 pointer SGPRs, spilled 120-770 SGPRs
+// into VGPR lanes and ran at one wave per SIMD (measured on MI355X, ResNet-50
+// group at K = 32: bfloat16 reduction 1.07 TB/s, binary32 fused step 3.9).
 #include "tc_internal.h"
 
 #ifndef TC_EW_THREADS
@@ -181,23 +186,38 @@ __device__ __forceinline__ void reduce_slots(const ReduceArgs<K, T>& a, I i, I d
     }
 }
 
-// Generic K (> kSpecialisedK): trees of 16 zero-padded, then a tree of the
-// at most TC_MAX_K/16 partial sums (zero-padded).
+// Generic K (> kSpecialisedK): the partial sums of the groups of 16 copies
+// (each a tree of 16, zero-padded) kept in four registers, +0 for a group
+// past k_total, and combined as the tree of four: (p0 + p1) + (p2 + p3).
+static_assert(TC_MAX_K == 4 * kSpecialisedK, "the generic kernels combine four groups of 16 copies");
+
+template <typename V>
+struct Parts {
+    V p0 = splat<V>(0.0f), p1 = splat<V>(0.0f), p2 = splat<V>(0.0f), p3 = splat<V>(0.0f);
+    __device__ __forceinline__ void set(int c, V p) {
+        p0 = c == 0 ? p : p0;
+        p1 = c == 1 ? p : p1;
+        p2 = c == 2 ? p : p2;
+        p3 = c == 3 ? p : p3;
+    }
+    __device__ __forceinline__ V sum() const { return (p0 + p1) + (p2 + p3); }
+};
+
 template <typename T, typename V, typename I>
 __device__ __forceinline__ void reduce_slot_generic(const ReduceArgs<TC_MAX_K, T>& a, I i) {
-    constexpr int kParts = TC_MAX_K / kSpecialisedK;
-    V part[kParts];
-#pragma unroll
-    for (int c = 0; c < kParts; ++c) {
+    Parts<V> parts;
+    const int groups = (a.k_total + kSpecialisedK - 1) / kSpecialisedK;
+#pragma unroll 1
+    for (int c = 0; c < groups; ++c) {
         V v[kSpecialisedK];
 #pragma unroll
         for (int q = 0; q < kSpecialisedK; ++q) {
             const int k = c * kSpecialisedK + q;
             v[q] = k < a.k_total ? Mem<V>::load(a.in[k], i) : splat<V>(0.0f);
         }
-        part[c] = Tree<kSpecialisedK>::sum(v);
+        parts.set(c, Tree<kSpecialisedK>::sum(v));
     }
-    V s = Tree<kParts>::sum(part);
+    V s = parts.sum();
     if (a.op == TC_AVG) s = s / splat<V>(static_cast<float>(a.k_total));
     Mem<V>::store(a.out, i, s);
 }
@@ -251,31 +271,35 @@ __device__ __forceinline__ void easgd_slots(const EasgdArgs<K, T>& a, I i, I du)
     }
 }
 
+// Generic K: per group of 16 workers, every load before the first store (a
+// store to one worker's buffer would otherwise order the next worker's loads
+// behind it).
 template <typename T, typename V, typename I>
 __device__ __forceinline__ void easgd_slot_generic(const EasgdArgs<TC_MAX_K, T>& a, I i) {
-    constexpr int kParts = TC_MAX_K / kSpecialisedK;
     const V c = Mem<V>::load(a.xc, i);
     const V rho = splat<V>(a.rho), neg_eta = splat<V>(-a.eta);
-    V part[kParts];
-#pragma unroll
-    for (int p = 0; p < kParts; ++p) {
-        V d[kSpecialisedK];
+    Parts<V> parts;
+    const int groups = (a.k_total + kSpecialisedK - 1) / kSpecialisedK;
+#pragma unroll 1
+    for (int p = 0; p < groups; ++p) {
+        V x[kSpecialisedK], g[kSpecialisedK], d[kSpecialisedK];
 #pragma unroll
         for (int q = 0; q < kSpecialisedK; ++q) {
             const int k = p * kSpecialisedK + q;
-            if (k < a.k_total) {
-                V x = Mem<V>::load(a.x[k], i);
-                const V g = Mem<V>::load(a.g[k], i);
-                d[q] = x - c;
-                x = fmav(neg_eta, fmav(rho, d[q], g), x);
-                Mem<V>::store(a.x[k], i, x);
-            } else {
-                d[q] = splat<V>(0.0f);
-            }
+            x[q] = k < a.k_total ? Mem<V>::load(a.x[k], i) : splat<V>(0.0f);
+            g[q] = k < a.k_total ? Mem<V>::load(a.g[k], i) : splat<V>(0.0f);
         }
-        part[p] = Tree<kSpecialisedK>::sum(d);
+#pragma unroll
+        for (int q = 0; q < kSpecialisedK; ++q) {
+            d[q] = p * kSpecialisedK + q < a.k_total ? x[q] - c : splat<V>(0.0f);  // +0 past k_total
+            x[q] = fmav(neg_eta, fmav(rho, d[q], g[q]), x[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < kSpecialisedK; ++q)
+            if (p * kSpecialisedK + q < a.k_total) Mem<V>::store(a.x[p * kSpecialisedK + q], i, x[q]);
+        parts.set(p, Tree<kSpecialisedK>::sum(d));
     }
-    Mem<V>::store(a.xc, i, fmav(splat<V>(a.a), Tree<kParts>::sum(part), c));
+    Mem<V>::store(a.xc, i, fmav(splat<V>(a.a), parts.sum(), c));
 }
 
 template <int K, typename T, int U, typename V, typename I>
@@ -333,23 +357,37 @@ struct SyncArgs {
 template <int K, typename T, int U, typename V, typename I>
 __device__ __forceinline__ void sync_slots(const SyncArgs<K, T>& a, I i, I du) {
     if constexpr (K == TC_MAX_K) {
-        constexpr int kParts = TC_MAX_K / kSpecialisedK;
-        V part[kParts];
-#pragma unroll
-        for (int c = 0; c < kParts; ++c) {
+        Parts<V> parts;
+        const int groups = (a.k_total + kSpecialisedK - 1) / kSpecialisedK;
+#pragma unroll 1
+        for (int c = 0; c < groups; ++c) {
             V v[kSpecialisedK];
 #pragma unroll
             for (int q = 0; q < kSpecialisedK; ++q) {
                 const int k = c * kSpecialisedK + q;
                 v[q] = k < a.k_total ? Mem<V>::load(static_cast<const T*>(a.g[k]), i) : splat<V>(0.0f);
             }
-            part[c] = Tree<kSpecialisedK>::sum(v);
+            parts.set(c, Tree<kSpecialisedK>::sum(v));
         }
-        const V S = Tree<kParts>::sum(part);
-        for (int q = 0; q < a.k_total; ++q) {
-            Mem<V>::store(a.x[q], i, fmav(splat<V>(-a.step), S, Mem<V>::load(a.x[q], i)));
-            if constexpr (sizeof(T) == 4)
-                if (a.broadcast) Mem<V>::store(a.g[q], i, S);
+        const V S = parts.sum();
+        // the workers in groups of 16, every load before the first store
+#pragma unroll 1
+        for (int c = 0; c < groups; ++c) {
+            V x[kSpecialisedK];
+#pragma unroll
+            for (int q = 0; q < kSpecialisedK; ++q) {
+                const int k = c * kSpecialisedK + q;
+                if (k < a.k_total) x[q] = Mem<V>::load(a.x[k], i);
+            }
+#pragma unroll
+            for (int q = 0; q < kSpecialisedK; ++q) {
+                const int k = c * kSpecialisedK + q;
+                if (k < a.k_total) {
+                    Mem<V>::store(a.x[k], i, fmav(splat<V>(-a.step), S, x[q]));
+                    if constexpr (sizeof(T) == 4)
+                        if (a.broadcast) Mem<V>::store(a.g[k], i, S);
+                }
+            }
         }
     } else {
         V g[U][K], x[U][K];
