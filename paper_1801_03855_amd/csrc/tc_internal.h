@@ -20,14 +20,20 @@ namespace tc {
 //   inside one tensor) move best in short chunks that a workgroup covers in
 //   one batch per lane; groups of many small tensors in longer chunks, which
 //   spread the per-chunk segment staging over more data (4,096: pack plus
-//   unpack 4% faster than with 8,192, 10% faster than with 2,048);
+//   unpack 4% faster than with 8,192, 10% faster than with 2,048), and
+//   2-byte elements on groups of large tensors in chunks of twice the
+//   elements (the bytes of a binary32 chunk);
 // - tensor-layout pack/unpack, whose workgroups move all K copies of a chunk:
 //   1,024 elements (against 2,048 and 512 on VGG-16's straight path, and
 //   against 512 and 2,048 to 8,192 on 10,000 small tensors), but 512 for
 //   the unpack through the tiles on groups of large tensors (ResNet-50:
-//   4-5% faster at K = 8, 8% at K = 16; the pack is 3% slower there);
+//   4-5% faster at K = 8, 8% at K = 16; the pack is 3% slower there), and
+//   the separate-buffer chunks at P <= 2 (except the direct binary32
+//   unpack at P = 2), where 1,024 elements move only 4-16 KB;
 // - the pipelined step: 512 elements (7-8% faster than 2,048 on ResNet-50,
-//   VGG-16 and 10,000 small tensors; 2% faster than 1,024 on the latter).
+//   VGG-16 and 10,000 small tensors; 2% faster than 1,024 on the latter),
+//   but the tensor-layout pack's 1,024 at P = 1, and at P = 2 except for
+//   binary32 gradients on the straight path.
 // All are multiples of every vector width (4, 8).
 #ifndef TC_PACK_CHUNK_LARGE
 #define TC_PACK_CHUNK_LARGE 2048
@@ -173,6 +179,7 @@ struct tc_group {
     tc_chunking tpack;             // tensor-layout pack/unpack
     tc_chunking tpack_fine;        // unpack through the tiles, large tensors
     tc_chunking pipe;              // the pipelined step
+    tc_chunking sep2;              // separate-buffer pack/unpack, 2-byte elements
     bool slot_bounds = false;      // every tensor boundary before the last,
                                    // partial slot is a multiple of 4
     int64_t* d_offsets = nullptr;

@@ -238,19 +238,20 @@ hipError_t run(const PackKernelArgs& a, int K, int64_t nchunks, hipStream_t s) {
 hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, bool /*flat_aligned*/,
                        hipStream_t stream) {
     const tc_group* g = tl->g;
+    const tc_chunking& c = tl->elem == 2 ? g->sep2 : g->sep;
     PackKernelArgs a{};
     a.offsets = g->d_offsets;
-    a.chunk_first = g->sep.d_first;
+    a.chunk_first = c.d_first;
     a.ptrs = tl->d_ptrs;
     a.n = g->n;
     a.N = g->N;
-    a.chunk = g->sep.chunk;
+    a.chunk = c.chunk;
     for (int k = 0; k < tl->K; ++k) a.flat[k] = flat[k];
     if (tl->elem == 2)
-        return unpack ? run<uint16_t, true>(a, tl->K, g->sep.nchunks, stream)
-                      : run<uint16_t, false>(a, tl->K, g->sep.nchunks, stream);
-    return unpack ? run<uint32_t, true>(a, tl->K, g->sep.nchunks, stream)
-                  : run<uint32_t, false>(a, tl->K, g->sep.nchunks, stream);
+        return unpack ? run<uint16_t, true>(a, tl->K, c.nchunks, stream)
+                      : run<uint16_t, false>(a, tl->K, c.nchunks, stream);
+    return unpack ? run<uint32_t, true>(a, tl->K, c.nchunks, stream)
+                  : run<uint32_t, false>(a, tl->K, c.nchunks, stream);
 }
 
 }  // namespace tc

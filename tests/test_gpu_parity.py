@@ -464,6 +464,17 @@ def test_pack_misaligned_tensors(orc, dtype):
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_pack_large_tensors_misaligned(orc, dtype):
+    """A group of large tensors (mean above 32,768 elements: 2,048-element
+    chunks, 4,096 for bfloat16), tensors one element into their allocations
+    and flat buffers one element past a 16-byte boundary: chunk edges inside
+    tensors, on both sides unaligned."""
+    sizes = [40001, 33335, 70002, 32769, 3]
+    _pack_roundtrip(orc, sizes, 3, dtype, misalign=True, seed=40)
+    _pack_roundtrip(orc, sizes, 2, dtype, misalign=True, seed=41, flat_shift=1)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("flat_shift", [1, 2, 3])
 def test_pack_misaligned_flat_buffers(orc, dtype, flat_shift):
     """Flat buffers 1-3 elements past a 16-byte boundary, tensors aligned and
