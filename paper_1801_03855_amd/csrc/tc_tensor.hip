@@ -347,9 +347,12 @@ struct TStepArgs {
     int K, flag;    // sync: broadcast the sum into g
     uint8_t order[TC_MAX_K];
     int R;
+    uint64_t exchanged;  // async: bit w set when worker w is in order[0..R)
 };
 
 enum class TOp { Sgd, Sync, Async };
+
+
 
 template <TOp OP, int P, typename T, typename I>
 __global__ __launch_bounds__(256) void tensor_step_kernel(TStepArgs<T> a) {
@@ -376,10 +379,45 @@ __global__ __launch_bounds__(256) void tensor_step_kernel(TStepArgs<T> a) {
             if constexpr (sizeof(T) == 4)
                 if (a.flag) store_slot(reinterpret_cast<float*>(a.g), piece, S);
         }
+    } else if constexpr (P >= 4) {
+        // The center's recurrence over the exchanges, c = fma(alpha, x_w - c,
+        // c) in order, is four scalar recurrences, one per component of the
+        // slot: lanes 0-3 of the slot's group run them, reading the exchanged
+        // worker's component from LDS and writing each step's difference to
+        // that worker's row of a second LDS array; each exchanged worker then
+        // takes its difference from its row.  (With all P lanes running the
+        // four-wide recurrence, the per-slot work grew as K^2: ALU-bound from
+        // K = 16 on.  Measured on MI355X against that, ResNet-50 group, R = K:
+        // K = 4 +23%, K = 16 +18%, K = 32 +59%, K = 64 +67%, K = 3 and 8
+        // level.)  The groups' rows are padded by one slot, so that the
+        // active lanes of a wave, reading or writing component i of the same
+        // worker in every group, fall in distinct LDS banks.
+        __shared__ f4 s_x[256 + 256 / P];
+        __shared__ f4 s_d[256 + 256 / P];
+        const f4 x = live ? load_slot(a.x, piece) : f4(0.0f);
+        const int row0 = (threadIdx.x & ~(P - 1)) + static_cast<int>(threadIdx.x) / P;  // the group's padded row 0
+        s_x[row0 + i] = x;
+        const float* xrow = reinterpret_cast<const float*>(s_x + row0) + i;
+        float* drow = reinterpret_cast<float*>(s_d + row0) + i;
+        const bool runs = slot && i < 4;
+        float c = runs ? __builtin_nontemporal_load(a.xc + (j * I(4) + I(i))) : 0.0f;
+        __syncthreads();
+        if (runs) {
+#pragma unroll 4
+            for (int r = 0; r < a.R; ++r) {
+                const int w4 = 4 * a.order[r];
+                const float d = xrow[w4] - c;
+                drow[w4] = d;
+                c = __builtin_fmaf(a.s0, d, c);
+            }
+            __builtin_nontemporal_store(c, a.xc + (j * I(4) + I(i)));
+        }
+        __syncthreads();
+        if (live && ((a.exchanged >> i) & 1)) store_slot(a.x, piece, fma4(f4(-a.s0), s_d[row0 + i], x));
     } else {
-        // every lane of the slot's group runs the center's recurrence over
-        // the exchanges, reading the exchanged worker's slot from LDS (one
-        // broadcast read per exchange)
+        // P <= 2: every lane of the slot's group runs the four-wide
+        // recurrence over the (at most 2) exchanges, reading the exchanged
+        // worker's slot from LDS
         __shared__ f4 s_x[256];
         const f4 x = live ? load_slot(a.x, piece) : f4(0.0f);
         f4 c = slot ? load_slot(a.xc, j) : f4(0.0f);
@@ -1549,7 +1587,10 @@ hipError_t tstep(int K, float* x, void* g, int g_dtype, float* xc, float s0, int
     }
     TStepArgs<float> a{};
     a.x = x; a.g = static_cast<float*>(g); a.xc = xc; a.nslot = n / 4; a.n = n; a.s0 = s0; a.K = K; a.flag = flag;
-    for (int r = 0; r < R; ++r) a.order[r] = static_cast<uint8_t>(order[r]);
+    for (int r = 0; r < R; ++r) {
+        a.order[r] = static_cast<uint8_t>(order[r]);
+        a.exchanged |= uint64_t(1) << order[r];
+    }
     a.R = R;
     return dispatch_tstep<OP, float>(a, s);
 }
