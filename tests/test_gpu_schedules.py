@@ -112,6 +112,30 @@ def test_elastic_async(orc, layout, K):
     assert_close(host_f32(xc), rc, span, f"{layout} K={K} x_c")
 
 
+@pytest.mark.parametrize("K,R", [(3, 3), (4, 2), (8, 8), (16, 16), (33, 20), (64, 64)])
+def test_elastic_async_layouts_bit_identical(orc, K, R):
+    """The tensor-layout exchange runs the center's recurrence once per
+    component (four lanes per slot) and hands each difference back through
+    LDS; the separate-buffer kernel runs it per element.  Both take the same
+    binary32 operations in the same order, so they agree bit for bit, every
+    worker (exchanged or not) and the center, on several workgroups and a
+    ragged tail."""
+    N = 4 * 3001 + 3
+    g = tc.Group([N])
+    xs = _copies(N, K, torch.float32, 300 + K, 0.05)
+    xc = torch.randn(N, generator=torch.Generator(device=DEV).manual_seed(8), device=DEV) * 0.05
+    order = [int(w) for w in np.random.default_rng(50 + K).permutation(K)[:R]]
+    Lt = Layout(orc, "tensor", g, K, xs)
+    xc_t = xc.clone()
+    tc.elastic_async_tensor(g, K, Lt.X, xc_t, order, 0.1125)
+    xs_s, xc_s = [t.clone() for t in xs], xc.clone()
+    tc.elastic_async(g, xs_s, xc_s, order, 0.1125)
+    torch.cuda.synchronize()
+    for i, got in enumerate(Lt.x_host()):
+        assert_bits_equal(got, host_f32(xs_s[i]), f"K={K} R={R} x[{i}] tensor vs separate")
+    assert_bits_equal(host_f32(xc_t), host_f32(xc_s), f"K={K} R={R} x_c tensor vs separate")
+
+
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("K", [1, 4, 8, 16, 64])
 def test_elastic_async_exact_regime(orc, layout, K):
