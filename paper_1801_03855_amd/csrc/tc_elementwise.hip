@@ -203,6 +203,12 @@ struct Parts {
     __device__ __forceinline__ V sum() const { return (p0 + p1) + (p2 + p3); }
 };
 
+// Every load of a group before its sums.  A full group of 16 copies loads
+// without conditions: a load under a condition compiled, for bfloat16
+// inputs, to a branch around it and a wait for it, one load in flight at a
+// time (measured on MI355X, ResNet-50 group: K = 17-64 4.1-4.2 TB/s, against
+// 5.8-6.2 without the conditions); a last, partial group keeps them and
+// loads only its copies (K = 17 in binary32: 9% faster than loading 16).
 template <typename T, typename V, typename I>
 __device__ __forceinline__ void reduce_slot_generic(const ReduceArgs<TC_MAX_K, T>& a, I i) {
     Parts<V> parts;
@@ -210,10 +216,15 @@ __device__ __forceinline__ void reduce_slot_generic(const ReduceArgs<TC_MAX_K, T
 #pragma unroll 1
     for (int c = 0; c < groups; ++c) {
         V v[kSpecialisedK];
+        if ((c + 1) * kSpecialisedK <= a.k_total) {
 #pragma unroll
-        for (int q = 0; q < kSpecialisedK; ++q) {
-            const int k = c * kSpecialisedK + q;
-            v[q] = k < a.k_total ? Mem<V>::load(a.in[k], i) : splat<V>(0.0f);
+            for (int q = 0; q < kSpecialisedK; ++q) v[q] = Mem<V>::load(a.in[c * kSpecialisedK + q], i);
+        } else {
+#pragma unroll
+            for (int q = 0; q < kSpecialisedK; ++q) {
+                const int k = c * kSpecialisedK + q;
+                v[q] = k < a.k_total ? Mem<V>::load(a.in[k], i) : splat<V>(0.0f);
+            }
         }
         parts.set(c, Tree<kSpecialisedK>::sum(v));
     }
