@@ -650,6 +650,11 @@ __device__ __forceinline__ void load_windows(const uintptr_t (&S)[N], u4 (&out)[
 #define TC_TPACK_WAVES_DIRECT 4
 #endif
 
+// Longer chunks are taken only while they still give 2,048 workgroups (8 per
+// CU): a group of 7,392 elements packed at K = 2 in 2 chunks of 4,096 took
+// 5.8 us, in 8 of 1,024 3.8 us.
+constexpr int64_t kMinLongerChunks = 2048;
+
 // Slots per LDS tile: the tile's pieces over P, at least 16, and no more
 // than the slots of a chunk (TC_TPACK_CHUNK / 4; tiles larger than the chunk
 // leave lanes idle), but at least one piece per lane (two for the bfloat16
@@ -1440,14 +1445,16 @@ hipError_t run_tpack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStre
     //   (2,048 or 4,096 elements; measured on MI355X, K = 1 and 2 on
     //   ResNet-50, VGG-16 and 10,000 small tensors: pack 2-80% faster,
     //   unpack 12-57% in bfloat16 and 20-35% for misaligned lists), except
-    //   the direct binary32 unpack at P = 2 (1-3% slower with them);
+    //   the direct binary32 unpack at P = 2 (1-3% slower with them), and
+    //   groups too small to fill the chip with them (kMinLongerChunks);
     // - unpack through the tiles, on a group of large tensors, takes the
     //   shorter chunking when a tile fits in its chunks (P >= 8; at P = 4
     //   the tiles would leave half the lanes idle).
     constexpr int fine_slots = TC_TPACK_CHUNK_FINE / 4;
     const bool fits = tl->elem == 2 ? tpack_tile_slots<P, 2, true>() <= fine_slots
                                     : tpack_tile_slots<P, 4, true>() <= fine_slots;
-    const bool longer = P <= 2 && !(DIRECT && unpack && tl->elem == 4 && P == 2);
+    const bool longer =
+        P <= 2 && !(DIRECT && unpack && tl->elem == 4 && P == 2) && g->sep.nchunks >= kMinLongerChunks;
     const tc_chunking& c = longer ? g->sep : unpack && !DIRECT && g->large && fits ? g->tpack_fine : g->tpack;
     TPackArgs a{g->d_offsets, c.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, c.chunk};
     dim3 grid(static_cast<unsigned>(c.nchunks));
@@ -1516,7 +1523,7 @@ constexpr bool pipe_direct_pays() { return (64 / P) * 4 * static_cast<int>(sizeo
 // buffer pack's chunks (2,048 or 4,096 elements) gained less at P <= 2.
 template <int P, typename T>
 hipError_t run_tpipe(const tc_group* g, TPipeArgs a, bool direct, hipStream_t stream) {
-    const bool longer = P == 1 || (P == 2 && !(direct && sizeof(T) == 4));
+    const bool longer = (P == 1 || (P == 2 && !(direct && sizeof(T) == 4))) && g->tpack.nchunks >= kMinLongerChunks;
     const tc_chunking& c = longer ? g->tpack : g->pipe;
     a.chunk_first = c.d_first;
     a.chunk = c.chunk;

@@ -177,7 +177,7 @@ def test_k_and_ragged_tail(orc, K):
 def test_misaligned_tensors(orc, K, gdt):
     """Every per-layer tensor one element into its allocation: the gather
     reads unaligned windows, the scatter writes whole granules inside runs,
-    with tile edges as run ends (K <= 2: the longer chunks)."""
+    with tile edges as run ends."""
     sizes = [513, 4099, 6, 70001, 3, 1030]
     _run(orc, sizes, K, gdt=gdt, seed=10 + K, misalign=True)
 
@@ -196,6 +196,18 @@ def test_slot_aligned_groups(orc, K, gdt):
     sizes = [4096, 8, 0, 12000, 516, 7]
     _run(orc, sizes, K, gdt=gdt, seed=70 + K)
     _run(orc, sizes, K, gdt=gdt, seed=80 + K, eta=0.125, rho=0.5, integer=True)
+
+
+@pytest.mark.parametrize("K,gdt,misalign", [(1, torch.float32, False), (1, torch.bfloat16, True),
+                                            (2, torch.bfloat16, False), (2, torch.float32, True),
+                                            (2, torch.float32, False)])
+def test_longer_chunks(orc, K, gdt, misalign):
+    """A group with enough 1,024-element chunks to fill the chip (2.2M
+    elements): at K = 1, and at K = 2 except binary32 gradients on the
+    straight path (the last case, which keeps 512), the step takes those
+    chunks, several tiles or straight steps per chunk."""
+    sizes = [700_000, 900_004, 600_000, 7] if not misalign else [700_001, 900_003, 600_002, 7]
+    _run(orc, sizes, K, gdt=gdt, seed=120 + K, misalign=misalign)
 
 
 @pytest.mark.parametrize("gdt", [torch.float32, torch.bfloat16])

@@ -118,10 +118,23 @@ def test_pack_tensor_large_tensors_tiled(orc, K, dtype):
     """A group of large tensors (mean above 32,768 elements) whose tensors
     start one element into their allocations and whose length is not a
     multiple of 4: the tiles, across many chunk edges inside each tensor,
-    in each chunking the kernels pick (the longer separate-buffer chunks at
-    K <= 2, the unpack's shorter tensor-layout chunks at K >= 8)."""
+    in the unpack's shorter tensor-layout chunks at K >= 8."""
     sizes = [40001, 33335, 70002, 32769]
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=60 + K, misalign=True)
+
+
+@pytest.mark.parametrize("K", [1, 2])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("misalign", [False, True])
+def test_pack_tensor_longer_chunks(orc, K, dtype, misalign):
+    """At K <= 2 a group with enough chunks to fill the chip (here 4.7M
+    elements of large tensors: 2,300 chunks of 2,048) packs and unpacks in
+    the separate-buffer chunks, several tiles per chunk; slot-multiple
+    sizes in their own allocations go straight through registers (but the
+    binary32 unpack at K = 2 keeps the short chunks), the same sizes one
+    element into their allocations through the tiles."""
+    sizes = [1_500_000, 1_200_004, 2_000_000, 9] if not misalign else [1_500_001, 1_200_003, 2_000_002, 9]
+    _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=90 + K, misalign=misalign)
 
 
 @pytest.mark.parametrize("K", [1, 2, 3, 4])
