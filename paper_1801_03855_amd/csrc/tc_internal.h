@@ -82,14 +82,19 @@ __device__ __forceinline__ void gst_nt(uintptr_t a, V v) {
     __builtin_nontemporal_store(v, reinterpret_cast<TC_GLOBAL V*>(a));
 }
 
-// A load at an address with no alignment beyond the element size: on
-// gfx950 global memory is accessed in unaligned mode, so a 16-byte (or
-// 8-byte) load at any byte address is one vector instruction, which the
+// A load or store at an address with no alignment beyond the element size:
+// on gfx950 global memory is accessed in unaligned mode, so a 16-byte (or
+// 8-byte) access at any byte address is one vector instruction, which the
 // memory pipeline splits over the cache lines it touches.
 template <typename V>
 __device__ __forceinline__ V gld_u(uintptr_t a) {
     typedef V Vu __attribute__((aligned(1)));
     return *reinterpret_cast<const TC_GLOBAL Vu*>(a);
+}
+template <typename V>
+__device__ __forceinline__ void gst_u(uintptr_t a, V v) {
+    typedef V Vu __attribute__((aligned(1)));
+    *reinterpret_cast<TC_GLOBAL Vu*>(a) = v;
 }
 
 // Workgroup w of a launch runs on XCD w % 8, and each of the 8 XCDs has its
