@@ -379,41 +379,6 @@ __global__ __launch_bounds__(256) void tensor_step_kernel(TStepArgs<T> a) {
             if constexpr (sizeof(T) == 4)
                 if (a.flag) store_slot(reinterpret_cast<float*>(a.g), piece, S);
         }
-    } else if constexpr (P >= 4) {
-        // The center's recurrence over the exchanges, c = fma(alpha, x_w - c,
-        // c) in order, is four scalar recurrences, one per component of the
-        // slot: lanes 0-3 of the slot's group run them, reading the exchanged
-        // worker's component from LDS and writing each step's difference to
-        // that worker's row of a second LDS array; each exchanged worker then
-        // takes its difference from its row.  (With all P lanes running the
-        // four-wide recurrence, the per-slot work grew as K^2: ALU-bound from
-        // K = 16 on.  Measured on MI355X against that, ResNet-50 group, R = K:
-        // K = 4 +23%, K = 16 +18%, K = 32 +59%, K = 64 +67%, K = 3 and 8
-        // level.)  The groups' rows are padded by one slot, so that the
-        // active lanes of a wave, reading or writing component i of the same
-        // worker in every group, fall in distinct LDS banks.
-        __shared__ f4 s_x[256 + 256 / P];
-        __shared__ f4 s_d[256 + 256 / P];
-        const f4 x = live ? load_slot(a.x, piece) : f4(0.0f);
-        const int row0 = (threadIdx.x & ~(P - 1)) + static_cast<int>(threadIdx.x) / P;  // the group's padded row 0
-        s_x[row0 + i] = x;
-        const float* xrow = reinterpret_cast<const float*>(s_x + row0) + i;
-        float* drow = reinterpret_cast<float*>(s_d + row0) + i;
-        const bool runs = slot && i < 4;
-        float c = runs ? __builtin_nontemporal_load(a.xc + (j * I(4) + I(i))) : 0.0f;
-        __syncthreads();
-        if (runs) {
-#pragma unroll 4
-            for (int r = 0; r < a.R; ++r) {
-                const int w4 = 4 * a.order[r];
-                const float d = xrow[w4] - c;
-                drow[w4] = d;
-                c = __builtin_fmaf(a.s0, d, c);
-            }
-            __builtin_nontemporal_store(c, a.xc + (j * I(4) + I(i)));
-        }
-        __syncthreads();
-        if (live && ((a.exchanged >> i) & 1)) store_slot(a.x, piece, fma4(f4(-a.s0), s_d[row0 + i], x));
     } else {
         // P <= 2: every lane of the slot's group runs the four-wide
         // recurrence over the (at most 2) exchanges, reading the exchanged
@@ -465,6 +430,85 @@ __global__ __launch_bounds__(256) void tensor_step_kernel(TStepArgs<T> a) {
                 }
                 a.xc[e] = c;
             }
+        }
+    }
+}
+
+// The asynchronous exchange at P >= 4.  The center's recurrence over the
+// exchanges, c = fma(alpha, x_w - c, c) in order, is four scalar
+// recurrences, one per component of a slot: lanes 0-3 of each slot's group
+// run them, reading the exchanged worker's component from LDS and writing
+// each step's difference to that worker's row of a second LDS array; each
+// exchanged worker then takes its difference from its row.  (With all P
+// lanes running the four-wide recurrence, the per-slot work grew as K^2:
+// ALU-bound from K = 16 on.  Measured on MI355X against that, ResNet-50
+// group, R = K: K = 4 +23%, K = 16 +18%, K = 32 +59%, K = 64 +67%, K = 3 and
+// 8 level.)  The groups' rows are padded by one slot, so that the active
+// lanes of a wave, reading or writing component i of the same worker in
+// every group, fall in distinct LDS banks.  A lane takes U = 2 slots, whose
+// recurrences interleave: with one, a kernel whose K is below P moved too
+// few bytes per wave (measured on MI355X against one slot: K = 3 +17%, K = 5
+// +35%, K = 8 +3%, K = 16 +5%, K = 32 +12%, VGG-16 K = 4 -3%; four slots
+// measured level or below two).
+template <int P, int U, typename I>
+__global__ __launch_bounds__(256) void tensor_async_kernel(TStepArgs<float> a) {
+    constexpr int SPW = 64 / P;
+    constexpr int ROWS = 256 + 256 / P;
+    const int K = a.K;
+    const int i = threadIdx.x % P;
+    const I j0 = first_slot<P, U, I>();
+    const I nslot = static_cast<I>(a.nslot);
+    __shared__ f4 s_x[U][ROWS];
+    __shared__ f4 s_d[U][ROWS];
+    const int row0 = (threadIdx.x & ~(P - 1)) + static_cast<int>(threadIdx.x) / P;  // the group's padded row 0
+    f4 x[U];
+    float c[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const I j = j0 + I(u) * SPW;
+        const bool slot = j < nslot;
+        x[u] = slot && i < K ? load_slot(a.x, j * I(K) + I(i)) : f4(0.0f);
+        c[u] = slot && i < 4 ? __builtin_nontemporal_load(a.xc + (j * I(4) + I(i))) : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) s_x[u][row0 + i] = x[u];
+    __syncthreads();
+    if (i < 4) {
+#pragma unroll 4
+        for (int r = 0; r < a.R; ++r) {
+            const int w = a.order[r];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const float d = reinterpret_cast<const float*>(&s_x[u][row0 + w])[i] - c[u];
+                reinterpret_cast<float*>(&s_d[u][row0 + w])[i] = d;
+                c[u] = __builtin_fmaf(a.s0, d, c[u]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const I j = j0 + I(u) * SPW;
+            if (j < nslot) __builtin_nontemporal_store(c[u], a.xc + (j * I(4) + I(i)));
+        }
+    }
+    __syncthreads();
+    if (i < K && ((a.exchanged >> i) & 1)) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const I j = j0 + I(u) * SPW;
+            if (j < nslot) store_slot(a.x, j * I(K) + I(i), fma4(f4(-a.s0), s_d[u][row0 + i], x[u]));
+        }
+    }
+    if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot, element by element
+        const int64_t e = 4 * a.nslot + threadIdx.x;
+        if (e < a.n) {
+            float ce = a.xc[e];
+            for (int r = 0; r < a.R; ++r) {
+                const int64_t k = (a.nslot * K + a.order[r]) * 4 + (e & 3);
+                const float d = a.x[k] - ce;
+                ce = __builtin_fmaf(a.s0, d, ce);
+                a.x[k] = __builtin_fmaf(-a.s0, d, a.x[k]);
+            }
+            a.xc[e] = ce;
         }
     }
 }
@@ -1564,15 +1608,29 @@ hipError_t launch_tensor_pipeline(const tc_tensorlist* grads, const tc_tensorlis
     }
 }
 
+#ifndef TC_TASYNC_U
+#define TC_TASYNC_U 2
+#endif
 template <TOp OP, int P, typename T>
 hipError_t run_tstep(const TStepArgs<T>& a, hipStream_t s) {
-    constexpr int SPB = 256 / P;
-    const int64_t blocks = (a.nslot + SPB - 1) / SPB;
-    dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
-    if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
-        hipLaunchKernelGGL((tensor_step_kernel<OP, P, T, uint32_t>), grid, dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL((tensor_step_kernel<OP, P, T, int64_t>), grid, dim3(256), 0, s, a);
+    if constexpr (OP == TOp::Async && P >= 4 && sizeof(T) == 4) {
+        constexpr int U = TC_TASYNC_U;
+        constexpr int SPB = 256 / P * U;
+        const int64_t blocks = (a.nslot + SPB - 1) / SPB;
+        dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+        if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
+            hipLaunchKernelGGL((tensor_async_kernel<P, U, uint32_t>), grid, dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL((tensor_async_kernel<P, U, int64_t>), grid, dim3(256), 0, s, a);
+    } else {
+        constexpr int SPB = 256 / P;
+        const int64_t blocks = (a.nslot + SPB - 1) / SPB;
+        dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+        if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
+            hipLaunchKernelGGL((tensor_step_kernel<OP, P, T, uint32_t>), grid, dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL((tensor_step_kernel<OP, P, T, int64_t>), grid, dim3(256), 0, s, a);
+    }
     return hipGetLastError();
 }
 
