@@ -396,9 +396,10 @@ def run_fused(tc, wl, w, sizes, g, steps, warmup):
     return out
 
 
-def _time_launches(fns, reps):
+def _time_launches(fns, reps, flush=None):
     """Median and minimum time (ms) of single launches, cycling through the
-    callables in fns (one per input set), from HIP events on the stream."""
+    callables in fns (one per input set), from HIP events on the stream;
+    flush, when given, runs before each launch, outside the timed interval."""
     import torch
 
     stream = torch.cuda.current_stream()
@@ -407,6 +408,8 @@ def _time_launches(fns, reps):
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
     torch.cuda.synchronize()
     for r in range(reps):
+        if flush is not None:
+            flush()
         ev[r][0].record(stream)
         fns[r % len(fns)]()
         ev[r][1].record(stream)
@@ -519,16 +522,19 @@ def config_table(tc, wl, reps=20):
     """Every configured workload's operations on both layouts: median and
     minimum time of single launches, algorithmic GB/s at the median and its
     fraction of peak.  The ResNet-50 K = 4 reduction (511 MB per call, about
-    twice the 256 MB last-level cache) is also timed cold, alternating between
-    two input sets; the tiny group is launch-bound, so only its times mean
-    anything there."""
+    twice the 256 MB last-level cache) is also timed cold: two sets of inputs
+    and output in turn, and before each call a 1 GiB copy with cacheable
+    loads and stores (outside the timed interval), so that no call finds its
+    inputs or its output left in that cache (non-temporal reads alone do not
+    evict an output written with cache-retaining stores); the tiny group is
+    launch-bound, so only its times mean anything there."""
     import torch
 
     dev = "cuda"
     out = {}
 
-    def row(nbytes, fns):
-        med, mn = _time_launches(fns, reps)
+    def row(nbytes, fns, flush=None):
+        med, mn = _time_launches(fns, reps, flush)
         gbs = nbytes / (med * 1e-3) / 1e9
         return {"ms_median": round(med, 5), "ms_min": round(mn, 5), "per_s": round(1e3 / med, 1),
                 "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
@@ -548,6 +554,12 @@ def config_table(tc, wl, reps=20):
             tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in gs]), G)
             gten.append(G)
         avg = torch.empty(N, device=dev)
+        avgs = [avg] + [torch.empty(N, device=dev) for _ in range(sets - 1)]
+        if sets > 1:
+            fl = (torch.empty(1 << 28, device=dev), torch.empty(1 << 28, device=dev))
+
+            def flush(fl=fl):
+                fl[1].copy_(fl[0])
         r = {"N": N, "K": K}
         for op in [o for o in ("reduce_sum", "reduce_avg") if o in w.ops]:
             kind = op.split("_")[1]
@@ -555,8 +567,10 @@ def config_table(tc, wl, reps=20):
             r[f"{op} separate"] = row(nb, [lambda gs=gs: tc.reduce(g, gs, avg, kind) for gs in gsep[:1]])
             r[f"{op} tensor"] = row(nb, [lambda G=G: tc.reduce_tensor(g, K, G, avg, kind) for G in gten[:1]])
             if sets > 1:
-                r[f"{op} separate, cold"] = row(nb, [lambda gs=gs: tc.reduce(g, gs, avg, kind) for gs in gsep])
-                r[f"{op} tensor, cold"] = row(nb, [lambda G=G: tc.reduce_tensor(g, K, G, avg, kind) for G in gten])
+                r[f"{op} separate, cold"] = row(nb, [lambda gs=gs, o=o: tc.reduce(g, gs, o, kind)
+                                                     for gs, o in zip(gsep, avgs)], flush)
+                r[f"{op} tensor, cold"] = row(nb, [lambda G=G, o=o: tc.reduce_tensor(g, K, G, o, kind)
+                                                   for G, o in zip(gten, avgs)], flush)
         if "easgd" in w.ops:
             xs, xc = wl.make_state(w, N, dev)
             X = torch.empty(tc.tensor_numel(g, K), device=dev)
@@ -574,7 +588,8 @@ def config_table(tc, wl, reps=20):
                 del grads, params
             del xs, xc, X, xc2
         out[wkey] = r
-        del gsep, gten, avg
+        del gsep, gten, avg, avgs
+        fl = flush = None
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
     return out

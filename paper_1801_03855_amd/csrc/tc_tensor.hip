@@ -126,6 +126,44 @@ __device__ __forceinline__ void store_slot(float* p, I s, f4 v) {
     __builtin_nontemporal_store(v, reinterpret_cast<f4*>(reinterpret_cast<char*>(p) + s * I(16)));
 }
 
+// Stores with explicit cache-policy bits (bit 0 sc0, bit 1 nt, bit 4 sc1) as
+// raw buffer stores when offsets are 32-bit; AUX < 0 keeps the plain
+// non-temporal global store.  Measured on MI355X with a 1 GiB copy between
+// calls (so that no call finds its output in the 256 MB last-level cache):
+// sc1 on the reduction's output -3% to +3% by group, on the step's center
+// +0 to +2%, on the workers and center together level; plain stores (0)
+// lost 13-16% on the step.  Called back to back without that copy, sc1 on
+// the reduction's output looked 4% faster on the groups whose output fits
+// in that cache: the output stayed there from one call to the next.  All
+// three keep non-temporal stores.
+#ifndef TC_TRD_STORE_AUX
+#define TC_TRD_STORE_AUX -1
+#endif
+#ifndef TC_TEA_X_STORE_AUX
+#define TC_TEA_X_STORE_AUX -1
+#endif
+#ifndef TC_TEA_C_STORE_AUX
+#define TC_TEA_C_STORE_AUX -1
+#endif
+template <int AUX, typename I>
+__device__ __forceinline__ void store_slot_pol(float* p, I s, f4 v) {
+    if constexpr (AUX >= 0 && sizeof(I) == 4) {
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(p, static_cast<short>(0), -1, 0x00020000);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), r, s * 16u, 0, AUX);
+    } else {
+        store_slot(p, s, v);
+    }
+}
+template <int AUX, typename I>
+__device__ __forceinline__ void store_elem_pol(float* p, I s, int comp, float v) {  // component comp of slot s
+    if constexpr (AUX >= 0 && sizeof(I) == 4) {
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(p, static_cast<short>(0), -1, 0x00020000);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, s * 16u + static_cast<uint32_t>(comp) * 4u, 0, AUX);
+    } else {
+        __builtin_nontemporal_store(v, reinterpret_cast<float*>(reinterpret_cast<char*>(p) + s * I(16)) + comp);
+    }
+}
+
 __device__ __forceinline__ float load_elem(const float* p, int64_t e) { return p[e]; }
 __device__ __forceinline__ float load_elem(const uint16_t* p, int64_t e) { return bf16_to_f32(p[e]); }
 
@@ -219,13 +257,11 @@ __global__ __launch_bounds__(256) void tensor_reduce_kernel(TReduceArgs<T> a) {
             // lanes 0-3 of the group hold one component each
             float s = split_group_sum<L>(v[u], threadIdx.x);
             if (a.op == TC_AVG) s = div_k<P>(s, K);
-            if (j < nslot && i < 4)
-                __builtin_nontemporal_store(s, reinterpret_cast<float*>(reinterpret_cast<char*>(a.out) + j * I(16)) +
-                                                   comp_of_lane(i));
+            if (j < nslot && i < 4) store_elem_pol<TC_TRD_STORE_AUX, I>(a.out, j, comp_of_lane(i), s);
         } else {
             f4 s = group_sum4<L>(v[u]);
             if (a.op == TC_AVG) s = div_k<P>(s, K);
-            if (j < nslot && i == 0) store_slot(a.out, j, s);
+            if (j < nslot && i == 0) store_slot_pol<TC_TRD_STORE_AUX, I>(a.out, j, s);
         }
     }
     if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot
@@ -300,8 +336,8 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
         const f4 d = live ? x[u] - c[u] : f4(0.0f);
         const f4 xn = fma4(neg_eta, fma4(rho, d, g[u]), x[u]);
         cn[u] = fma4(alpha, group_sum4<P>(d), c[u]);
-        if (live) store_slot(a.x, j * I(K) + I(i), xn);
-        if (!kShare && j < nslot && i == 0) store_slot(a.xc, j, cn[u]);
+        if (live) store_slot_pol<TC_TEA_X_STORE_AUX, I>(a.x, j * I(K) + I(i), xn);
+        if (!kShare && j < nslot && i == 0) store_slot_pol<TC_TEA_C_STORE_AUX, I>(a.xc, j, cn[u]);
     }
     if constexpr (kShare) {
         // lane m < WS stores slot jw + m, whose new center slot group m % SPW
@@ -312,7 +348,8 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
             const f4 t = shfl4(cn[u], (lane % SPW) * P);
             if (lane / SPW == u) out = t;
         }
-        if (lane < WS && jw + static_cast<I>(lane) < nslot) store_slot(a.xc, jw + static_cast<I>(lane), out);
+        if (lane < WS && jw + static_cast<I>(lane) < nslot)
+            store_slot_pol<TC_TEA_C_STORE_AUX, I>(a.xc, jw + static_cast<I>(lane), out);
     }
     if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot
         const int64_t e = 4 * a.nslot + threadIdx.x;
