@@ -122,6 +122,13 @@ __device__ __forceinline__ uint32_t tile_of(uint32_t b, uint32_t nb) {
     }
 }
 
+// A tensor's start relative to a chunk's first element, clamped to the
+// chunk [0, clen]: the chunk-relative segment bounds the pack, unpack and
+// pipelined kernels stage.
+__device__ __forceinline__ int32_t clamp_rel(int64_t v, int32_t clen) {
+    return static_cast<int32_t>(v < 0 ? 0 : (v > clen ? clen : v));
+}
+
 // Records a printf-style message as this thread's last error.
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();

@@ -49,10 +49,6 @@ struct PackKernelArgs {
     void* flat[TC_MAX_K];
 };
 
-__device__ __forceinline__ int32_t clamp_rel(int64_t v, int32_t clen) {
-    return static_cast<int32_t>(v < 0 ? 0 : (v > clen ? clen : v));
-}
-
 // Destination byte range [d0, d1) of one segment's part of the chunk, and
 // the displacement from a destination byte to its source byte.
 struct SegView {

@@ -598,10 +598,6 @@ struct TPackArgs {
     int64_t N, chunk;
 };
 
-__device__ __forceinline__ int32_t clamp_rel(int64_t v, int32_t clen) {
-    return static_cast<int32_t>(v < 0 ? 0 : (v > clen ? clen : v));
-}
-
 // Bytes [sh, sh + 16) of the 32-byte little-endian concatenation lo:hi.
 __device__ __forceinline__ u4 funnel(u4 lo, u4 hi, uint32_t sh) {
     const uint32_t w[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
