@@ -685,8 +685,8 @@ __device__ __forceinline__ void load_windows(const uintptr_t (&S)[N], u4 (&out)[
 }
 
 // Workgroup b moves chunk b of all K copies through LDS, M slots at a time
-// (M = 1024/P, at least 16: a 16 KB tile for binary32), so that both global
-// sides are contiguous:
+// (tpack_tile_slots: 1,024 or 2,048 pieces over P, at least 16 slots, at
+// most a chunk's), so that both global sides are contiguous:
 //   per-copy side  lanes take consecutive slots of one copy (M*SB bytes of
 //                  one copy per wave instruction when M >= 64);
 //   tensor side    lanes take consecutive pieces in tensor order.
