@@ -137,6 +137,16 @@ def test_pack_tensor_longer_chunks(orc, K, dtype, misalign):
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=90 + K, misalign=misalign)
 
 
+@pytest.mark.parametrize("K", [1, 2])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_pack_tensor_longer_chunks_small_tensors(orc, K, dtype):
+    """The same at K <= 2 for a group of small slot-multiple tensors (1,700
+    log-uniform sizes rounded up to multiples of 4, 8.8M elements: 2,148
+    chunks of 4,096), chunks holding many tensor boundaries."""
+    sizes = [(v + 3) // 4 * 4 for v in wl.many_small_sizes(1700, seed=13)] + [5]
+    _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=95 + K)
+
+
 @pytest.mark.parametrize("K", [1, 2, 3, 4])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_large_tensors_slot_aligned(orc, K, dtype):
