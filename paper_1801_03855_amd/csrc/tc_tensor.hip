@@ -596,6 +596,7 @@ struct TPackArgs {
     void* tensor;       // tensor layout, K copies
     int32_t n, K;
     int64_t N, chunk;
+    int32_t groups;     // workgroups per chunk, each taking P of the K copies
 };
 
 // Bytes [sh, sh + 16) of the 32-byte little-endian concatenation lo:hi.
@@ -721,6 +722,9 @@ __device__ __forceinline__ void load_windows(const uintptr_t (&S)[N], u4 (&out)[
 #ifndef TC_TPACK_DIRECT
 #define TC_TPACK_DIRECT 1
 #endif
+#ifndef TC_TPACK_GROUP_BYTES
+#define TC_TPACK_GROUP_BYTES 128
+#endif
 // The direct binary32 pack and unpack are compiled for at least 4 waves per
 // SIMD (amdgpu_waves_per_eu; they already run at 6, so the hint takes no
 // occupancy): measured on MI355X, VGG-16 at K = 4 packs 3% and unpacks 2%
@@ -762,11 +766,16 @@ void tensor_pack_kernel(TPackArgs a) {
     __shared__ uintptr_t s_base[kMaxStage];
     // one row more than a tile: unpack keeps the next tile's first slot there
     __shared__ __attribute__((aligned(16))) unsigned char s_tile[(M + 1) * ROW];
-    const int K = a.K;
-    const int64_t cstart = static_cast<int64_t>(blockIdx.x) * a.chunk;
+    // workgroup (chunk, group): copies [kg0, kg0 + K) of chunk, K <= P; the
+    // tensor layout's stride is all a.K copies
+    const int KS = a.K;
+    const int chunk = static_cast<int>(blockIdx.x) / a.groups;
+    const int kg0 = (static_cast<int>(blockIdx.x) - chunk * a.groups) * P;
+    const int K = KS - kg0 < P ? KS - kg0 : P;
+    const int64_t cstart = static_cast<int64_t>(chunk) * a.chunk;
     const int32_t clen = static_cast<int32_t>(a.N - cstart < a.chunk ? a.N - cstart : a.chunk);
-    const int32_t lo = a.chunk_first[blockIdx.x];
-    const int32_t hi = a.chunk_first[blockIdx.x + 1];
+    const int32_t lo = a.chunk_first[chunk];
+    const int32_t hi = a.chunk_first[chunk + 1];
     const int nseg = hi - lo + 1;
     const int64_t first_start = a.offsets[lo] - cstart;
     const bool rel_staged = nseg <= kMaxStage;
@@ -774,7 +783,7 @@ void tensor_pack_kernel(TPackArgs a) {
     auto rel_global = [&](int s) -> int32_t { return clamp_rel(a.offsets[lo + s] - cstart, clen); };
     auto base_global = [&](int kk, int s) -> uintptr_t {
         const int64_t st = s == 0 ? first_start : a.offsets[lo + s] - cstart;
-        return reinterpret_cast<uintptr_t>(a.ptrs[static_cast<int64_t>(kk) * a.n + lo + s]) -
+        return reinterpret_cast<uintptr_t>(a.ptrs[static_cast<int64_t>(kg0 + kk) * a.n + lo + s]) -
                static_cast<uintptr_t>(st * ES);
     };
     if (rel_staged)
@@ -795,7 +804,7 @@ void tensor_pack_kernel(TPackArgs a) {
     const uintptr_t tens = reinterpret_cast<uintptr_t>(a.tensor);
     const int64_t slot0 = cstart / 4;
     auto piece = [&](int js, int kk) -> uintptr_t {
-        return tens + static_cast<uintptr_t>(((slot0 + js) * K + kk) * SB);
+        return tens + static_cast<uintptr_t>(((slot0 + js) * KS + kg0 + kk) * SB);
     };
     auto tile = [&](int jl, int kk) -> unsigned char* { return s_tile + jl * ROW + kk * SB; };
     const int nsl = clen / 4;  // whole slots in this chunk
@@ -1018,7 +1027,7 @@ void tensor_pack_kernel(TPackArgs a) {
         int s = find(je);
         while (je >= rel(s + 1)) ++s;
         const uintptr_t t = base(kk, s) + static_cast<uintptr_t>(je) * ES;
-        const uintptr_t pc = tens + static_cast<uintptr_t>((((slot0 + nsl) * K + kk) * 4 + e) * ES);
+        const uintptr_t pc = tens + static_cast<uintptr_t>((((slot0 + nsl) * KS + kg0 + kk) * 4 + e) * ES);
         if (UNPACK) gst<T>(t, gld<T>(pc));
         else gst<T>(pc, gld<T>(t));
     }
@@ -1538,8 +1547,9 @@ hipError_t run_tpack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStre
     const bool longer =
         P <= 2 && !(DIRECT && unpack && tl->elem == 4 && P == 2) && g->sep.nchunks >= kMinLongerChunks;
     const tc_chunking& c = longer ? g->sep : unpack && !DIRECT && g->large && fits ? g->tpack_fine : g->tpack;
-    TPackArgs a{g->d_offsets, c.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, c.chunk};
-    dim3 grid(static_cast<unsigned>(c.nchunks));
+    const int groups = (tl->K + P - 1) / P;
+    TPackArgs a{g->d_offsets, c.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, c.chunk, groups};
+    dim3 grid(static_cast<unsigned>(c.nchunks * groups));
     if (tl->elem == 2) {
         if (unpack) hipLaunchKernelGGL((tensor_pack_kernel<P, uint16_t, true, DIRECT>), grid, dim3(256), 0, stream, a);
         else hipLaunchKernelGGL((tensor_pack_kernel<P, uint16_t, false, DIRECT>), grid, dim3(256), 0, stream, a);
@@ -1562,7 +1572,19 @@ hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack
     // wave; VGG-16 +15%, ResNet-50 +17%) and lose at K = 2 (up to 19%).
     const bool direct = TC_TPACK_DIRECT && (64 / next_pow2(tl->K)) * 4 * tl->elem >= 256 && g->slot_bounds &&
                         tl->slot_aligned;
-    switch (next_pow2(tl->K)) {
+    // Through the tiles at P = 16 and 32, the copies are taken in groups whose
+    // part of a slot row is TC_TPACK_GROUP_BYTES (one 128-byte line: 8
+    // binary32 or 16 bfloat16 copies), each group by a workgroup of its own,
+    // whose tile, registers and per-copy side are those of P = 8 (or 16).
+    // Measured on MI355X against one workgroup for all K copies: the
+    // 10,000-tensor group's binary32 unpack +12% at K = 16 and +6.5% at
+    // K = 32 (its bfloat16 pack +2% at K = 32), ResNet-50 and VGG-16 at K =
+    // 16 and 32 level to +3%; at K = 64 up to 4% slower, and groups of 64
+    // bytes (half lines) 11-33% slower everywhere.
+    const int pg = TC_TPACK_GROUP_BYTES / (4 * tl->elem);
+    const int pk = next_pow2(tl->K);
+    const int pt = !direct && pg > 0 && pk > pg && pk <= 32 ? pg : pk;
+    switch (pt) {
 #define TC_CASE(p) \
     case p: return direct ? run_tpack<p, true>(tl, tensor, unpack, stream) \
                           : run_tpack<p, false>(tl, tensor, unpack, stream);

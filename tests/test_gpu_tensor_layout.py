@@ -91,16 +91,18 @@ def test_pack_tensor_resnet50(orc, dtype):
     _tensor_pack_roundtrip(orc, wl.group_sizes("resnet50"), 8, dtype, seed=1)
 
 
-@pytest.mark.parametrize("K", [1, 3, 5, 16, 17, 64])
+@pytest.mark.parametrize("K", [1, 3, 5, 9, 16, 17, 24, 31, 64])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_ragged_and_misaligned(orc, K, dtype):
     """Lengths not multiples of 4 (a partial last slot), tensors starting
-    one element past their allocation, zero-size tensors."""
+    one element past their allocation, zero-size tensors; K = 9-31 take the
+    copies in groups of one 128-byte line of each slot row (binary32 K > 8,
+    bfloat16 K > 16), the last group partial."""
     sizes = [3, 0, 5, 4097, 1, 2, 0, 250, 7]
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=K, misalign=True)
 
 
-@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 16, 64])
+@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 12, 16, 32, 64])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_slot_aligned(orc, K, dtype):
     """Slot-multiple tensor lengths before a ragged last tensor, tensors in
@@ -112,7 +114,7 @@ def test_pack_tensor_slot_aligned(orc, K, dtype):
     _tensor_pack_roundtrip(orc, sizes, K, dtype, seed=30 + K, misalign=True)
 
 
-@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 16])
+@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 16, 20])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_pack_tensor_large_tensors_tiled(orc, K, dtype):
     """A group of large tensors (mean above 32,768 elements) whose tensors
