@@ -172,6 +172,16 @@ def test_k_and_ragged_tail(orc, K):
     _run(orc, sizes, K, seed=K)
 
 
+@pytest.mark.parametrize("sizes", [[1], [3], [2, 1], [5], [4, 3]])
+@pytest.mark.parametrize("K,gdt", [(1, torch.float32), (3, torch.bfloat16), (16, torch.float32)])
+def test_groups_of_at_most_one_slot(orc, sizes, K, gdt):
+    """Groups of at most one whole slot: the tail launch alone (N < 4) or
+    one slot and a tail, on both paths (slot-aligned lists and lists one
+    element into their allocations)."""
+    _run(orc, sizes, K, gdt=gdt, seed=sum(sizes) * 10 + K)
+    _run(orc, sizes, K, gdt=gdt, seed=sum(sizes) * 10 + K + 1, misalign=True)
+
+
 @pytest.mark.parametrize("K,gdt", [(1, torch.float32), (2, torch.float32), (2, torch.bfloat16), (3, torch.float32),
                                    (8, torch.float32), (16, torch.bfloat16), (5, torch.bfloat16)])
 def test_misaligned_tensors(orc, K, gdt):

@@ -238,6 +238,40 @@ def test_tensor_integer_inputs_bit_exact(orc, K):
     assert_exact(host_f32(xc), rc, f"K={K} x_c")
 
 
+@pytest.mark.parametrize("N", [1, 2, 3, 5, 7])
+@pytest.mark.parametrize("K", [1, 3, 16])
+def test_tensor_layout_groups_smaller_than_a_slot(orc, N, K):
+    """Groups of at most one whole slot: the kernels' element-by-element
+    tails alone (N < 4) or one slot and a tail.  Reduction and step against
+    the oracle, pack and unpack bit for bit, in both gradient types."""
+    g = tc.Group([N])
+    for dtype in (torch.float32, torch.bfloat16):
+        _tensor_pack_roundtrip(orc, [N], K, dtype, seed=N * 100 + K, misalign=True)
+        gs = _make_copies(N, K, dtype, seed=N * 10 + K, scale=0.01)
+        hg = _to_tensor_layout(orc, gs, 0)
+        G = _device_tensor(hg, dtype)
+        gcopies = orc.copies_from_tensor(hg, K, N)
+        out = torch.empty(N, device=DEV)
+        tc.reduce_tensor(g, K, G, out, "avg")
+        xs = _make_copies(N, K, torch.float32, seed=N * 10 + K + 1, scale=0.05)
+        hx = _to_tensor_layout(orc, xs, 0)
+        X = _device_tensor(hx, torch.float32)
+        xc = torch.randn(N, generator=torch.Generator(device=DEV).manual_seed(N + K), device=DEV) * 0.05
+        h_c = host_f32(xc)
+        tc.easgd_step_tensor(g, K, X, G, xc, 0.05, 2.25)
+        torch.cuda.synchronize()
+        assert_close(host_f32(out), orc.reduce(gcopies, oracle.AVG), reduce_mag(gcopies, True), f"N={N} K={K} avg")
+        h_x = orc.copies_from_tensor(hx, K, N)
+        rx = [a.astype(np.float64) for a in h_x]
+        rc = h_c.astype(np.float64)
+        mx, mc = easgd_mags(h_x, gcopies, h_c, 0.05, 2.25)
+        orc.easgd_step(rx, gcopies, rc, 0.05, 2.25)
+        got = orc.copies_from_tensor(host_f32(X), K, N)
+        for i in range(K):
+            assert_close(got[i], rx[i], mx[i], f"N={N} K={K} {dtype} x[{i}]")
+        assert_close(host_f32(xc), rc, mc, f"N={N} K={K} {dtype} x_c")
+
+
 # ------------------------------------------------------------------- easgd
 
 @pytest.mark.parametrize("K,gdt", [(1, torch.float32), (2, torch.float32), (3, torch.bfloat16), (4, torch.float32),
