@@ -197,6 +197,23 @@ int32_t easgd_step_ex(const tc_group* g, int32_t K, float* const* x,
                       float eta, float rho, void* stream);
 
 /* ------------------------------------------------------------------------
+ * reduce_easgd_step: the K-way reduction of the gradients (the push's sum
+ * over the tensors of a key, Sec. 3.2, and its average as SGD.Update's
+ * rescale gives it, Sec. 5) fused with the elastic step above (Sec. 2.2,
+ * Eqs. 2 and 3, summed over K workers, with the SGD move of Sec. 2.1), in
+ * one pass that reads each gradient once.  Equivalent, bit for bit, to
+ *     tc_reduce_ex(g, K, grad, g_dtype, out, op);
+ *     easgd_step_ex(g, K, x, grad, g_dtype, x_c, eta, rho);
+ * (the sums use the same pairwise tree, AVG the same single rounding of
+ * SUM / K).  Arguments as easgd_step_ex, plus out: device pointer to N
+ * binary32 values (written), overlapping none of x, grad, x_c; op: TC_SUM
+ * or TC_AVG.  TC_EINVAL on bad arguments, NULL out with N > 0 included.
+ * ---------------------------------------------------------------------- */
+int32_t reduce_easgd_step(const tc_group* g, int32_t K, float* const* x,
+                          const void* const* grad, int32_t g_dtype, float* x_c,
+                          float* out, int32_t op, float eta, float rho, void* stream);
+
+/* ------------------------------------------------------------------------
  * Tensor layout.  The paper's "tensor" (Sec. 6.1) collects one vector per
  * worker and treats the set as a single unit.  In this layout the K
  * copies of a group live in ONE buffer, interleaved in slots of four
@@ -242,6 +259,14 @@ int32_t tc_reduce_tensor(const tc_group* g, int32_t K, const void* in, int32_t i
  * buffers must not overlap. */
 int32_t easgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad,
                           int32_t g_dtype, float* x_c, float eta, float rho, void* stream);
+
+/* reduce_easgd_step on tensor-layout workers and gradients: bit for bit
+ * tc_reduce_tensor(g, K, grad, g_dtype, out, op) followed by
+ * easgd_step_tensor(g, K, x, grad, g_dtype, x_c, eta, rho).  out: N binary32
+ * values, 16-byte aligned, overlapping none of x, grad, x_c. */
+int32_t reduce_easgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad,
+                                 int32_t g_dtype, float* x_c, float* out, int32_t op,
+                                 float eta, float rho, void* stream);
 
 /* ------------------------------------------------------------------------
  * The ESGD schedule with a communication period (Sec. 5, the ESGD listing:

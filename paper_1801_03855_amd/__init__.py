@@ -85,11 +85,13 @@ def lib(path: str = LIBRARY) -> ctypes.CDLL:
         "tc_reduce_ex": (i32, [_VP, i32, _VPP, i32, _VP, i32, _VP]),
         "easgd_step": (i32, [_VP, i32, _VPP, _VPP, _VP, f32, f32, _VP]),
         "easgd_step_ex": (i32, [_VP, i32, _VPP, _VPP, i32, _VP, f32, f32, _VP]),
+        "reduce_easgd_step": (i32, [_VP, i32, _VPP, _VPP, i32, _VP, _VP, i32, f32, f32, _VP]),
         "tc_tensor_numel": (i64, [_VP, i32]),
         "tc_pack_tensor": (i32, [_VP, _VP, _VP]),
         "tc_unpack_tensor": (i32, [_VP, _VP, _VP]),
         "tc_reduce_tensor": (i32, [_VP, i32, _VP, i32, _VP, i32, _VP]),
         "easgd_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, _VP, f32, f32, _VP]),
+        "reduce_easgd_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, _VP, _VP, i32, f32, f32, _VP]),
         "sgd_step": (i32, [_VP, i32, _VPP, _VPP, i32, f32, _VP]),
         "sgd_step_tensor": (i32, [_VP, i32, _VP, _VP, i32, f32, _VP]),
         "easgd_period_step": (i32, [_VP, i32, _VPP, _VPP, i32, _VP, f32, f32, i64, i32, _VP]),
@@ -252,6 +254,24 @@ def easgd_step(group: Group, xs: Sequence[torch.Tensor], gs: Sequence[torch.Tens
                                _stream(stream)))
 
 
+def reduce_easgd_step(group: Group, xs: Sequence[torch.Tensor], gs: Sequence[torch.Tensor], xc: torch.Tensor,
+                      out: torch.Tensor, eta: float, rho: float, op="avg", stream=None) -> None:
+    """The sum (or average) of the gradients into out and the fused step on
+    xs and xc, in one pass (reduce_easgd_step)."""
+    n = group.numel
+    if len(xs) != len(gs):
+        raise ValueError("need one gradient per worker")
+    gdt = gs[0].dtype
+    if gdt not in _DTYPES:
+        raise TypeError(f"gradients have dtype {gdt}")
+    xp = _ptr_array([_dev_ptr(t, n, (torch.float32,), f"x[{i}]") for i, t in enumerate(xs)])
+    gp = _ptr_array([_dev_ptr(t, n, (gdt,), f"grad[{i}]") for i, t in enumerate(gs)])
+    _check(lib().reduce_easgd_step(group.handle, len(xs), xp, gp, _DTYPES[gdt],
+                                   _dev_ptr(xc, n, (torch.float32,), "x_c"),
+                                   _dev_ptr(out, n, (torch.float32,), "out"), _OPS[op], float(eta), float(rho),
+                                   _stream(stream)))
+
+
 # --------------------------------------------------------------- tensor layout
 
 def tensor_numel(group: Group, K: int) -> int:
@@ -295,6 +315,21 @@ def easgd_step_tensor(group: Group, K: int, x: torch.Tensor, g: torch.Tensor, xc
                                    _dev_ptr(g, n, (gdt,), "grad"), _DTYPES[gdt],
                                    _dev_ptr(xc, group.numel, (torch.float32,), "x_c"), float(eta), float(rho),
                                    _stream(stream)))
+
+
+def reduce_easgd_step_tensor(group: Group, K: int, x: torch.Tensor, g: torch.Tensor, xc: torch.Tensor,
+                             out: torch.Tensor, eta: float, rho: float, op="avg", stream=None) -> None:
+    """reduce_easgd_step on tensor-layout workers x and gradients g
+    (reduce_easgd_step_tensor)."""
+    n = tensor_numel(group, K)
+    gdt = g.dtype
+    if gdt not in _DTYPES:
+        raise TypeError(f"gradients have dtype {gdt}")
+    _check(lib().reduce_easgd_step_tensor(group.handle, K, _dev_ptr(x, n, (torch.float32,), "x"),
+                                          _dev_ptr(g, n, (gdt,), "grad"), _DTYPES[gdt],
+                                          _dev_ptr(xc, group.numel, (torch.float32,), "x_c"),
+                                          _dev_ptr(out, group.numel, (torch.float32,), "out"), _OPS[op],
+                                          float(eta), float(rho), _stream(stream)))
 
 
 # ----------------------------------------------- schedules and synchronous SGD

@@ -266,34 +266,57 @@ TC_API int32_t tc_reduce(const tc_group* g, int32_t K, const float* const* in, f
 
 // ------------------------------------------------------------------ easgd
 
-TC_API int32_t easgd_step_ex(const tc_group* g, int32_t K, float* const* x, const void* const* grad,
-                             int32_t g_dtype, float* x_c, float eta, float rho, void* stream) {
+// The step alone (fused false; out and op unused), or fused with the
+// reduction of the gradients into out.
+static int32_t easgd_common(const tc_group* g, int32_t K, float* const* x, const void* const* grad, int32_t g_dtype,
+                            float* x_c, bool fused, float* out, int32_t op, float eta, float rho, void* stream,
+                            const char* what) {
     clear_error();
     if (!g) return fail(TC_EINVAL, "group is NULL");
     if (K < 1 || K > TC_MAX_K) { set_error("K = %d outside [1, %d]", K, TC_MAX_K); return TC_EINVAL; }
     const int es = elem_size(g_dtype);
     if (!es) { set_error("unknown dtype %d", g_dtype); return TC_EINVAL; }
+    if (fused && op != TC_SUM && op != TC_AVG) { set_error("unknown op %d", op); return TC_EINVAL; }
     if (!std::isfinite(eta) || !std::isfinite(rho)) return fail(TC_EINVAL, "eta and rho must be finite");
     if (int32_t r = check_device(g)) return r;
     if (g->N == 0) return TC_OK;
-    if (!x || !grad || !x_c) return fail(TC_EINVAL, "NULL buffer");
+    if (!x || !grad || !x_c || (fused && !out)) return fail(TC_EINVAL, "NULL buffer");
     const int64_t xb = g->N * 4, gb = g->N * es;
     if (!aligned(x_c, 4)) return fail(TC_EINVAL, "x_c is not 4-byte aligned");
     bool vec = aligned(x_c, 16);
+    if (out) {
+        if (!aligned(out, 4)) return fail(TC_EINVAL, "out is not 4-byte aligned");
+        if (overlap(out, xb, x_c, xb)) return fail(TC_EINVAL, "out overlaps x_c");
+        vec = vec && aligned(out, 16);
+    }
     for (int32_t i = 0; i < K; ++i) {
         if (!x[i] || !grad[i]) { set_error("x[%d] or grad[%d] is NULL", i, i); return TC_EINVAL; }
         if (!aligned(x[i], 4) || !aligned(grad[i], es)) { set_error("x[%d] or grad[%d] misaligned", i, i); return TC_EINVAL; }
         vec = vec && aligned(x[i], 16) && aligned(grad[i], es == 4 ? 16 : 8);
         if (overlap(x[i], xb, x_c, xb)) { set_error("x[%d] overlaps x_c", i); return TC_EINVAL; }
         if (overlap(grad[i], gb, x_c, xb)) { set_error("grad[%d] overlaps x_c", i); return TC_EINVAL; }
+        if (out && overlap(out, xb, x[i], xb)) { set_error("out overlaps x[%d]", i); return TC_EINVAL; }
+        if (out && overlap(out, xb, grad[i], gb)) { set_error("out overlaps grad[%d]", i); return TC_EINVAL; }
         for (int32_t q = 0; q < K; ++q) {
             if (q < i && overlap(x[i], xb, x[q], xb)) { set_error("x[%d] overlaps x[%d]", i, q); return TC_EINVAL; }
             if (overlap(grad[q], gb, x[i], xb)) { set_error("grad[%d] overlaps x[%d]", q, i); return TC_EINVAL; }
         }
     }
-    hipError_t e = launch_easgd(K, x, grad, g_dtype, x_c, eta, rho, g->N, vec, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "easgd_step launch");
+    hipError_t e = launch_easgd(K, x, grad, g_dtype, x_c, out, op, eta, rho, g->N, vec,
+                                static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, what);
     return TC_OK;
+}
+
+TC_API int32_t easgd_step_ex(const tc_group* g, int32_t K, float* const* x, const void* const* grad,
+                             int32_t g_dtype, float* x_c, float eta, float rho, void* stream) {
+    return easgd_common(g, K, x, grad, g_dtype, x_c, false, nullptr, TC_SUM, eta, rho, stream, "easgd_step launch");
+}
+
+TC_API int32_t reduce_easgd_step(const tc_group* g, int32_t K, float* const* x, const void* const* grad,
+                                 int32_t g_dtype, float* x_c, float* out, int32_t op, float eta, float rho,
+                                 void* stream) {
+    return easgd_common(g, K, x, grad, g_dtype, x_c, true, out, op, eta, rho, stream, "reduce_easgd_step launch");
 }
 
 TC_API int32_t easgd_step(const tc_group* g, int32_t K, float* const* x, const float* const* grad, float* x_c,
@@ -347,26 +370,45 @@ TC_API int32_t tc_reduce_tensor(const tc_group* g, int32_t K, const void* in, in
     return TC_OK;
 }
 
-TC_API int32_t easgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad, int32_t g_dtype,
-                                 float* x_c, float eta, float rho, void* stream) {
+// As easgd_common, on tensor-layout buffers.
+static int32_t tensor_easgd_common(const tc_group* g, int32_t K, float* x, const void* grad, int32_t g_dtype,
+                                   float* x_c, bool fused, float* out, int32_t op, float eta, float rho,
+                                   void* stream, const char* what) {
     clear_error();
     if (!g) return fail(TC_EINVAL, "group is NULL");
     if (K < 1 || K > TC_MAX_K) { set_error("K = %d outside [1, %d]", K, TC_MAX_K); return TC_EINVAL; }
     const int es = elem_size(g_dtype);
     if (!es) { set_error("unknown dtype %d", g_dtype); return TC_EINVAL; }
+    if (fused && op != TC_SUM && op != TC_AVG) { set_error("unknown op %d", op); return TC_EINVAL; }
     if (!std::isfinite(eta) || !std::isfinite(rho)) return fail(TC_EINVAL, "eta and rho must be finite");
     if (int32_t r = check_device(g)) return r;
     if (g->N == 0) return TC_OK;
-    if (!x || !grad || !x_c) return fail(TC_EINVAL, "NULL buffer");
-    if (!aligned(x, 16) || !aligned(grad, 16) || !aligned(x_c, 16))
+    if (!x || !grad || !x_c || (fused && !out)) return fail(TC_EINVAL, "NULL buffer");
+    if (!aligned(x, 16) || !aligned(grad, 16) || !aligned(x_c, 16) || (out && !aligned(out, 16)))
         return fail(TC_EINVAL, "tensor-layout calls need 16-byte aligned buffers");
     const int64_t tn = tc_tensor_numel(g, K);
     if (overlap(x, tn * 4, grad, tn * es)) return fail(TC_EINVAL, "x overlaps grad");
     if (overlap(x, tn * 4, x_c, g->N * 4)) return fail(TC_EINVAL, "x overlaps x_c");
     if (overlap(grad, tn * es, x_c, g->N * 4)) return fail(TC_EINVAL, "grad overlaps x_c");
-    hipError_t e = launch_tensor_easgd(K, x, grad, g_dtype, x_c, eta, rho, g->N, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "easgd_step_tensor launch");
+    if (out && (overlap(out, g->N * 4, x, tn * 4) || overlap(out, g->N * 4, grad, tn * es) ||
+                overlap(out, g->N * 4, x_c, g->N * 4)))
+        return fail(TC_EINVAL, "out overlaps x, grad or x_c");
+    hipError_t e = launch_tensor_easgd(K, x, grad, g_dtype, x_c, out, op, eta, rho, g->N,
+                                       static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, what);
     return TC_OK;
+}
+
+TC_API int32_t easgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad, int32_t g_dtype,
+                                 float* x_c, float eta, float rho, void* stream) {
+    return tensor_easgd_common(g, K, x, grad, g_dtype, x_c, false, nullptr, TC_SUM, eta, rho, stream,
+                               "easgd_step_tensor launch");
+}
+
+TC_API int32_t reduce_easgd_step_tensor(const tc_group* g, int32_t K, float* x, const void* grad, int32_t g_dtype,
+                                        float* x_c, float* out, int32_t op, float eta, float rho, void* stream) {
+    return tensor_easgd_common(g, K, x, grad, g_dtype, x_c, true, out, op, eta, rho, stream,
+                               "reduce_easgd_step_tensor launch");
 }
 
 // ------------------------------------------- schedules and synchronous SGD

@@ -249,11 +249,22 @@ struct EasgdArgs {
     uint32_t bytes;     // size of each x buffer and of xc when below 4 GiB
     float eta, rho, a;  // a = eta*rho rounded to binary32
     int k_total;
+    static constexpr bool kReduce = false;
 };
 
-template <int K, typename T, int U, typename V, typename I>
-__device__ __forceinline__ void easgd_slots(const EasgdArgs<K, T>& a, I i, I du) {
-    V c[U], x[U][K], g[U][K];
+// The step fused with the K-way reduction of the gradients it reads: out =
+// the SUM (or AVG) of g_0 .. g_{K-1}, by the reduction's own tree and
+// quotient, so the result is bit for bit that of the reduction call.
+template <int K, typename T>
+struct ReduceEasgdArgs : EasgdArgs<K, T> {
+    float* out;
+    int op;
+    static constexpr bool kReduce = true;
+};
+
+template <int K, typename T, int U, typename V, typename I, typename A>
+__device__ __forceinline__ void easgd_slots(const A& a, I i, I du) {
+    V c[U], x[U][K], g[U][K], r[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         c[u] = Mem<V>::load(a.xc, i + I(u) * du);
@@ -273,23 +284,28 @@ __device__ __forceinline__ void easgd_slots(const EasgdArgs<K, T>& a, I i, I du)
             x[u][q] = fmav(neg_eta, fmav(rho, d[q], g[u][q]), x[u][q]);
         }
         c[u] = fmav(alpha, Tree<K>::sum(d), c[u]);
+        if constexpr (A::kReduce) {
+            r[u] = Tree<K>::sum(g[u]);
+            if (a.op == TC_AVG) r[u] = r[u] / splat<V>(static_cast<float>(K));
+        }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
 #pragma unroll
         for (int q = 0; q < K; ++q) store_pol<TC_EA_X_STORE_AUX, V, I>(a.x[q], i + I(u) * du, x[u][q], a.bytes);
         store_pol<TC_EA_C_STORE_AUX, V, I>(a.xc, i + I(u) * du, c[u], a.bytes);
+        if constexpr (A::kReduce) store_pol<TC_RD_STORE_AUX, V, I>(a.out, i + I(u) * du, r[u], a.bytes);
     }
 }
 
 // Generic K: per group of 16 workers, every load before the first store (a
 // store to one worker's buffer would otherwise order the next worker's loads
 // behind it).
-template <typename T, typename V, typename I>
-__device__ __forceinline__ void easgd_slot_generic(const EasgdArgs<TC_MAX_K, T>& a, I i) {
+template <typename T, typename V, typename I, typename A>
+__device__ __forceinline__ void easgd_slot_generic(const A& a, I i) {
     const V c = Mem<V>::load(a.xc, i);
     const V rho = splat<V>(a.rho), neg_eta = splat<V>(-a.eta);
-    Parts<V> parts;
+    Parts<V> parts, gparts;
     const int groups = (a.k_total + kSpecialisedK - 1) / kSpecialisedK;
 #pragma unroll 1
     for (int p = 0; p < groups; ++p) {
@@ -309,12 +325,19 @@ __device__ __forceinline__ void easgd_slot_generic(const EasgdArgs<TC_MAX_K, T>&
         for (int q = 0; q < kSpecialisedK; ++q)
             if (p * kSpecialisedK + q < a.k_total) Mem<V>::store(a.x[p * kSpecialisedK + q], i, x[q]);
         parts.set(p, Tree<kSpecialisedK>::sum(d));
+        // the gradients past k_total are +0, as in the reduction's last group
+        if constexpr (A::kReduce) gparts.set(p, Tree<kSpecialisedK>::sum(g));
     }
     Mem<V>::store(a.xc, i, fmav(splat<V>(a.a), parts.sum(), c));
+    if constexpr (A::kReduce) {
+        V s = gparts.sum();
+        if (a.op == TC_AVG) s = s / splat<V>(static_cast<float>(a.k_total));
+        Mem<V>::store(a.out, i, s);
+    }
 }
 
-template <int K, typename T, int U, typename V, typename I>
-__device__ __forceinline__ void easgd_any(const EasgdArgs<K, T>& a, I i, I du) {
+template <int K, typename T, int U, typename V, typename I, typename A>
+__device__ __forceinline__ void easgd_any(const A& a, I i, I du) {
     if constexpr (K == TC_MAX_K) easgd_slot_generic<T, V, I>(a, i);
     else easgd_slots<K, T, U, V, I>(a, i, du);
 }
@@ -485,6 +508,10 @@ __device__ __forceinline__ void op_any(const ReduceArgs<K, T>& a, I i, I du) { r
 template <int K, typename T, int U, typename V, typename I>
 __device__ __forceinline__ void op_any(const EasgdArgs<K, T>& a, I i, I du) { easgd_any<K, T, U, V, I>(a, i, du); }
 template <int K, typename T, int U, typename V, typename I>
+__device__ __forceinline__ void op_any(const ReduceEasgdArgs<K, T>& a, I i, I du) {
+    easgd_any<K, T, U, V, I>(a, i, du);
+}
+template <int K, typename T, int U, typename V, typename I>
 __device__ __forceinline__ void op_any(const SgdArgs<K, T>& a, I i, I du) { sgd_slots<K, T, U, V, I>(a, i, du); }
 template <int K, typename T, int U, typename V, typename I>
 __device__ __forceinline__ void op_any(const SyncArgs<K, T>& a, I i, I du) { sync_slots<K, T, U, V, I>(a, i, du); }
@@ -581,9 +608,9 @@ hipError_t run_reduce(const void* const* in, float* out, int op, int k_total, in
 }
 
 template <int K, typename T>
-hipError_t run_easgd(float* const* x, const void* const* g, float* xc, float eta, float rho, int k_total,
-                     int64_t n, bool vec, hipStream_t s) {
-    EasgdArgs<K, T> a{};
+hipError_t run_easgd(float* const* x, const void* const* g, float* xc, float* out, int op, float eta, float rho,
+                     int k_total, int64_t n, bool vec, hipStream_t s) {
+    ReduceEasgdArgs<K, T> a{};
     for (int q = 0; q < k_total; ++q) {
         a.x[q] = x[q];
         a.g[q] = static_cast<const T*>(g[q]);
@@ -594,7 +621,10 @@ hipError_t run_easgd(float* const* x, const void* const* g, float* xc, float eta
     a.rho = rho;
     a.a = eta * rho;  // one binary32 rounding, on the host
     a.k_total = k_total;
-    return launch<K, T, easgd_unroll(K)>(a, n, vec, 4, s);
+    a.out = out;
+    a.op = op;
+    if (out) return launch<K, T, easgd_unroll(K)>(a, n, vec, 4, s);
+    return launch<K, T, easgd_unroll(K)>(static_cast<const EasgdArgs<K, T>&>(a), n, vec, 4, s);
 }
 
 #define TC_FOR_K(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)
@@ -611,14 +641,14 @@ hipError_t dispatch_reduce(int K, const void* const* in, float* out, int op, int
 }
 
 template <typename T>
-hipError_t dispatch_easgd(int K, float* const* x, const void* const* g, float* xc, float eta, float rho, int64_t n,
-                          bool vec, hipStream_t s) {
+hipError_t dispatch_easgd(int K, float* const* x, const void* const* g, float* xc, float* out, int op, float eta,
+                          float rho, int64_t n, bool vec, hipStream_t s) {
     switch (K) {
 #define TC_CASE(k) \
-    case k: return run_easgd<k, T>(x, g, xc, eta, rho, K, n, vec, s);
+    case k: return run_easgd<k, T>(x, g, xc, out, op, eta, rho, K, n, vec, s);
         TC_FOR_K(TC_CASE)
 #undef TC_CASE
-        default: return run_easgd<TC_MAX_K, T>(x, g, xc, eta, rho, K, n, vec, s);
+        default: return run_easgd<TC_MAX_K, T>(x, g, xc, out, op, eta, rho, K, n, vec, s);
     }
 }
 
@@ -817,10 +847,10 @@ hipError_t launch_reduce(int K, const void* const* in, int in_dtype, float* out,
     return dispatch_reduce<float>(K, in, out, op, n, vector_ok, stream);
 }
 
-hipError_t launch_easgd(int K, float* const* x, const void* const* g, int g_dtype, float* xc, float eta, float rho,
-                        int64_t n, bool vector_ok, hipStream_t stream) {
-    if (g_dtype == TC_BF16) return dispatch_easgd<uint16_t>(K, x, g, xc, eta, rho, n, vector_ok, stream);
-    return dispatch_easgd<float>(K, x, g, xc, eta, rho, n, vector_ok, stream);
+hipError_t launch_easgd(int K, float* const* x, const void* const* g, int g_dtype, float* xc, float* out, int op,
+                        float eta, float rho, int64_t n, bool vector_ok, hipStream_t stream) {
+    if (g_dtype == TC_BF16) return dispatch_easgd<uint16_t>(K, x, g, xc, out, op, eta, rho, n, vector_ok, stream);
+    return dispatch_easgd<float>(K, x, g, xc, out, op, eta, rho, n, vector_ok, stream);
 }
 
 }  // namespace tc

@@ -137,7 +137,9 @@ void clear_error();
 // caller; these only pick a kernel and enqueue it on `stream`.
 hipError_t launch_reduce(int K, const void* const* in, int in_dtype, float* out, int op,
                          int64_t n, bool vector_ok, hipStream_t stream);
-hipError_t launch_easgd(int K, float* const* x, const void* const* g, int g_dtype, float* xc,
+// out == nullptr: the step alone; otherwise the step fused with the
+// reduction of the gradients into out (op TC_SUM or TC_AVG).
+hipError_t launch_easgd(int K, float* const* x, const void* const* g, int g_dtype, float* xc, float* out, int op,
                         float eta, float rho, int64_t n, bool vector_ok, hipStream_t stream);
 
 hipError_t launch_sgd(int K, float* const* x, const void* const* g, int g_dtype, float eta, int64_t n, bool vector_ok,
@@ -155,8 +157,8 @@ hipError_t launch_pack(const tc_tensorlist* tl, void* const* flat, bool unpack, 
 // Tensor layout (K copies interleaved in slots of 4 elements).
 hipError_t launch_tensor_reduce(int K, const void* in, int in_dtype, float* out, int op, int64_t n,
                                 hipStream_t stream);
-hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, float* xc, float eta, float rho,
-                               int64_t n, hipStream_t stream);
+hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, float* xc, float* out, int op, float eta,
+                               float rho, int64_t n, hipStream_t stream);
 hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStream_t stream);
 hipError_t launch_tensor_sgd(int K, float* x, const void* g, int g_dtype, float eta, int64_t n, hipStream_t s);
 hipError_t launch_tensor_sync_sgd(int K, float* x, void* g, int g_dtype, float eta, float rescale, int broadcast,

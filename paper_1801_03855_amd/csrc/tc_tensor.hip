@@ -288,6 +288,8 @@ struct TEasgdArgs {
     int64_t nslot, n;
     float eta, rho, a;
     int K;
+    float* out;      // RED: N values, the SUM (op TC_SUM) or AVG of the K gradients
+    int op;
 };
 
 // A wave of the step covers WS = U * 64 / P consecutive slots.  At P >= 16
@@ -300,7 +302,9 @@ __device__ __forceinline__ f4 shfl4(f4 v, int src) {
     return f4{__shfl(v.x, src, 64), __shfl(v.y, src, 64), __shfl(v.z, src, 64), __shfl(v.w, src, 64)};
 }
 
-template <int P, typename T, int U, typename I>
+// RED: the step fused with the reduction of the gradients it reads, by the
+// reduction kernel's own butterflies and quotient (bit for bit its result).
+template <int P, typename T, int U, typename I, bool RED>
 __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
     constexpr int SPW = 64 / P;
     constexpr int WS = U * SPW;
@@ -338,6 +342,18 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
         cn[u] = fma4(alpha, group_sum4<P>(d), c[u]);
         if (live) store_slot_pol<TC_TEA_X_STORE_AUX, I>(a.x, j * I(K) + I(i), xn);
         if (!kShare && j < nslot && i == 0) store_slot_pol<TC_TEA_C_STORE_AUX, I>(a.xc, j, cn[u]);
+        if constexpr (RED) {
+            // the gradients of lanes past K, and of slots past the end, are +0
+            if constexpr (P >= 4) {
+                float r = split_group_sum<P>(g[u], threadIdx.x);
+                if (a.op == TC_AVG) r = div_k<P>(r, K);
+                if (j < nslot && i < 4) store_elem_pol<TC_TRD_STORE_AUX, I>(a.out, j, comp_of_lane(i), r);
+            } else {
+                f4 r = group_sum4<P>(g[u]);
+                if (a.op == TC_AVG) r = div_k<P>(r, K);
+                if (j < nslot && i == 0) store_slot_pol<TC_TRD_STORE_AUX, I>(a.out, j, r);
+            }
+        }
     }
     if constexpr (kShare) {
         // lane m < WS stores slot jw + m, whose new center slot group m % SPW
@@ -355,19 +371,26 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
         const int64_t e = 4 * a.nslot + threadIdx.x;
         if (e < a.n) {
             const float cv = a.xc[e];
-            float d[P];
+            float d[P], gt[P];
 #pragma unroll
             for (int q = 0; q < P; ++q) {
                 if (q < K) {
                     const int64_t idx = (a.nslot * K + q) * 4 + (e & 3);
                     const float xv = a.x[idx];
+                    gt[q] = load_elem(a.g, idx);
                     d[q] = xv - cv;
-                    a.x[idx] = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, d[q], load_elem(a.g, idx)), xv);
+                    a.x[idx] = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, d[q], gt[q]), xv);
                 } else {
                     d[q] = 0.0f;
+                    gt[q] = 0.0f;
                 }
             }
             a.xc[e] = __builtin_fmaf(a.a, Tree<P>::sum(d), cv);
+            if constexpr (RED) {
+                float r = Tree<P>::sum(gt);
+                if (a.op == TC_AVG) r = div_k<P>(r, K);
+                a.out[e] = r;
+            }
         }
     }
 }
@@ -1474,18 +1497,24 @@ hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hip
     return run_treduce_as<P, T, false>(K, in, out, op, n, s);
 }
 
-template <int P, typename T>
-hipError_t run_teasgd(int K, float* x, const void* g, float* xc, float eta, float rho, int64_t n, hipStream_t s) {
+template <int P, typename T, bool RED>
+hipError_t run_teasgd_as(const TEasgdArgs<T>& a, hipStream_t s) {
     constexpr int U = teasgd_unroll(P);
     constexpr int SPB = 256 / P;
-    TEasgdArgs<T> a{x, static_cast<const T*>(g), xc, n / 4, n, eta, rho, eta * rho, K};
     const int64_t blocks = (a.nslot + SPB * U - 1) / (SPB * U);
     dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
-    if ((a.nslot + 1) * K * 16 < (int64_t(1) << 32))
-        hipLaunchKernelGGL((tensor_easgd_kernel<P, T, U, uint32_t>), grid, dim3(256), 0, s, a);
+    if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
+        hipLaunchKernelGGL((tensor_easgd_kernel<P, T, U, uint32_t, RED>), grid, dim3(256), 0, s, a);
     else
-        hipLaunchKernelGGL((tensor_easgd_kernel<P, T, U, int64_t>), grid, dim3(256), 0, s, a);
+        hipLaunchKernelGGL((tensor_easgd_kernel<P, T, U, int64_t, RED>), grid, dim3(256), 0, s, a);
     return hipGetLastError();
+}
+
+template <int P, typename T>
+hipError_t run_teasgd(int K, float* x, const void* g, float* xc, float* out, int op, float eta, float rho, int64_t n,
+                      hipStream_t s) {
+    TEasgdArgs<T> a{x, static_cast<const T*>(g), xc, n / 4, n, eta, rho, eta * rho, K, out, op};
+    return out ? run_teasgd_as<P, T, true>(a, s) : run_teasgd_as<P, T, false>(a, s);
 }
 
 #define TC_FOR_P(X) X(1) X(2) X(4) X(8) X(16) X(32) X(64)
@@ -1502,11 +1531,11 @@ hipError_t dispatch_treduce(int K, const void* in, float* out, int op, int64_t n
 }
 
 template <typename T>
-hipError_t dispatch_teasgd(int K, float* x, const void* g, float* xc, float eta, float rho, int64_t n,
-                           hipStream_t s) {
+hipError_t dispatch_teasgd(int K, float* x, const void* g, float* xc, float* out, int op, float eta, float rho,
+                           int64_t n, hipStream_t s) {
     switch (next_pow2(K)) {
 #define TC_CASE(p) \
-    case p: return run_teasgd<p, T>(K, x, g, xc, eta, rho, n, s);
+    case p: return run_teasgd<p, T>(K, x, g, xc, out, op, eta, rho, n, s);
         TC_FOR_P(TC_CASE)
 #undef TC_CASE
         default: return hipErrorInvalidValue;
@@ -1521,10 +1550,10 @@ hipError_t launch_tensor_reduce(int K, const void* in, int in_dtype, float* out,
     return dispatch_treduce<float>(K, in, out, op, n, stream);
 }
 
-hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, float* xc, float eta, float rho,
-                               int64_t n, hipStream_t stream) {
-    if (g_dtype == TC_BF16) return dispatch_teasgd<uint16_t>(K, x, g, xc, eta, rho, n, stream);
-    return dispatch_teasgd<float>(K, x, g, xc, eta, rho, n, stream);
+hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, float* xc, float* out, int op, float eta,
+                               float rho, int64_t n, hipStream_t stream) {
+    if (g_dtype == TC_BF16) return dispatch_teasgd<uint16_t>(K, x, g, xc, out, op, eta, rho, n, stream);
+    return dispatch_teasgd<float>(K, x, g, xc, out, op, eta, rho, n, stream);
 }
 
 template <int P, bool DIRECT>

@@ -66,6 +66,8 @@ def test_null_handles_are_rejected(L):
     assert L.tc_reduce_ex(None, 2, arr, 0, None, 0, None) == tc.TC_EINVAL
     assert L.easgd_step(None, 2, arr, arr, None, 0.1, 0.5, None) == tc.TC_EINVAL
     assert L.easgd_step_ex(None, 2, arr, arr, 1, None, 0.1, 0.5, None) == tc.TC_EINVAL
+    assert L.reduce_easgd_step(None, 2, arr, arr, 0, None, None, 1, 0.1, 0.5, None) == tc.TC_EINVAL
+    assert L.reduce_easgd_step_tensor(None, 2, None, None, 0, None, None, 1, 0.1, 0.5, None) == tc.TC_EINVAL
     assert L.tc_pack(None, arr, None) == tc.TC_EINVAL
     assert L.tc_unpack(None, arr, None) == tc.TC_EINVAL
     assert not L.tc_tensorlist_create(None, 1, arr, 0)

@@ -1,11 +1,12 @@
 """Buffers of 4 GiB and more: every kernel switches from 32-bit byte offsets to
 64-bit indices there.  Separate buffers of 2^30 + 1000 binary32 elements, and
 a tensor layout of K = 4 copies of 2^28 + 10 elements (a ragged last slot),
-through reduce, the fused step, pack/unpack and the one-launch pipeline.
-Sampled positions (random, around element 2^30 and byte 2^32 of each buffer,
-and the last ones) are checked against the oracle; pack/unpack and the
-pipeline bit for bit against their definitions and the four calls.  About
-35 GB of device memory in total.
+through reduce, the fused step, the reduction fused with the step,
+pack/unpack and the one-launch pipeline.  Sampled positions (random, around
+element 2^30 and byte 2^32 of each buffer, and the last ones) are checked
+against the oracle; pack/unpack, the fused reduction and step, and the
+pipeline bit for bit against their definitions and the separate calls.
+About 40 GB of device memory in total.
 """
 
 import numpy as np
@@ -55,10 +56,19 @@ def test_separate_buffers_beyond_4gib(orc):
     h_g = [host_f32(t[ti]) for t in gs]
     h_x = [host_f32(t[ti]) for t in xs]
     h_c = host_f32(xc[ti])
+    xs2, xc2 = [t.clone() for t in xs], xc.clone()
     avg = torch.empty(N, device=DEV)
     tc.reduce(g, gs, avg, "avg")
     tc.easgd_step(g, xs, gs, xc, ETA, RHO)
+    # the same as one call, bit for bit
+    avg2 = torch.empty(N, device=DEV)
+    tc.reduce_easgd_step(g, xs2, gs, xc2, avg2, ETA, RHO, "avg")
     torch.cuda.synchronize()
+    assert torch.equal(avg2.view(torch.int32), avg.view(torch.int32))
+    assert torch.equal(xc2.view(torch.int32), xc.view(torch.int32))
+    for i in range(K):
+        assert torch.equal(xs2[i].view(torch.int32), xs[i].view(torch.int32)), i
+    del xs2, xc2, avg2
     assert_close(host_f32(avg[ti]), orc.reduce(h_g, oracle.AVG), reduce_mag(h_g, True), "avg beyond 4 GiB")
     rx = [a.astype(np.float64) for a in h_x]
     rc = h_c.astype(np.float64)
@@ -99,6 +109,7 @@ def test_tensor_layout_beyond_4gib(orc):
     tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
     del xs
     Xp, xcp = X.clone(), xc.clone()
+    Xf, xcf = X.clone(), xc.clone()
     # the four calls
     tc.pack_tensor(grads, G)
     gbar = torch.empty(N, device=DEV)
@@ -106,8 +117,14 @@ def test_tensor_layout_beyond_4gib(orc):
     tc.easgd_step_tensor(g, K, X, G, xc, ETA, RHO)
     outs = [torch.empty(N, device=DEV) for _ in range(K)]
     tc.unpack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in outs]), X)
+    # the reduction and the step as one call, bit for bit
+    gbarf = torch.empty(N, device=DEV)
+    tc.reduce_easgd_step_tensor(g, K, Xf, G, xcf, gbarf, ETA, RHO, "avg")
     torch.cuda.synchronize()
-    del G
+    assert torch.equal(gbarf.view(torch.int32), gbar.view(torch.int32))
+    assert torch.equal(xcf.view(torch.int32), xc.view(torch.int32))
+    assert torch.equal(Xf.view(torch.int32), X.view(torch.int32))
+    del G, Xf, xcf, gbarf
     # the same step as one launch (packed gradients not written)
     gbarp = torch.empty(N, device=DEV)
     params = [torch.empty(N, device=DEV) for _ in range(K)]
