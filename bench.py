@@ -56,6 +56,11 @@ WORKLOADS = {
     # the 8-tensor group at K = 2 (7,392 elements): bound by launch and host
     # overhead, selectable so that a kernel trace can split the two
     "tiny_k2_pipeline": ("tiny_k2", ("pack", "reduce", "easgd", "unpack"), "tensor"),
+    # the same steps with the reduction and the step as one call
+    # (reduce_easgd_step): three calls per step
+    "resnet50_k8_fused": ("resnet50_k8_easgd", ("pack", "reduce_easgd", "unpack"), "tensor"),
+    "vgg16_k4_fused": ("vgg16_k4_easgd", ("pack", "reduce_easgd", "unpack"), "tensor"),
+    "many_small_k16_bf16_fused": ("many_small_k16_bf16", ("pack", "reduce_easgd", "unpack"), "tensor"),
 }
 LAYOUTS = ("tensor", "separate")
 
@@ -68,6 +73,8 @@ def op_bytes(op: str, K: int, N: int, s_g: int) -> int:
         return (K * s_g + 4) * N
     if op == "easgd":     # read+write K workers and the center, read K gradients
         return ((8 + s_g) * K + 8) * N
+    if op == "reduce_easgd":  # the step's bytes and the binary32 average written
+        return ((8 + s_g) * K + 12) * N
     if op == "unpack":    # read K flat workers, write K per-layer copies
         return 2 * K * N * 4
     raise ValueError(op)
@@ -205,6 +212,7 @@ def cpu_baseline(wkey: str, ops, sample_elems: int = 30_000_000, min_seconds: fl
             orc.unpack(x, sub)
         t["unpack"] += time.perf_counter() - t0
         reps += 1
+    t["reduce_easgd"] = t["reduce"] + t["easgd"]  # the oracle defines it as the two
     secs = sum(t[o] for o in ops)
     nbytes = reps * sum(op_bytes(o, w.K, n, s_g) for o in ops)
     out = {"value": round(nbytes / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
@@ -285,6 +293,8 @@ def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
                 tc.reduce_tensor(g, K, G, gbar, "avg", stream)
             elif op == "easgd":
                 tc.easgd_step_tensor(g, K, X, G, xc, w.eta, w.rho, stream)
+            elif op == "reduce_easgd":
+                tc.reduce_easgd_step_tensor(g, K, X, G, xc, gbar, w.eta, w.rho, "avg", stream)
             elif op == "unpack":
                 tc.unpack_tensor(x_tl, X, stream)
     else:
@@ -297,6 +307,8 @@ def run_pipeline(tc, wl, w, sizes, g, ops, layout, steps, warmup, name):
                 tc.reduce(g, gflat, gbar, "avg", stream)
             elif op == "easgd":
                 tc.easgd_step(g, xs, gflat, xc, w.eta, w.rho, stream)
+            elif op == "reduce_easgd":
+                tc.reduce_easgd_step(g, xs, gflat, xc, gbar, w.eta, w.rho, "avg", stream)
             elif op == "unpack":
                 tc.unpack(x_tl, xs, stream)
 
@@ -392,6 +404,51 @@ def run_fused(tc, wl, w, sizes, g, steps, warmup):
         torch.cuda.synchronize()
         out[write_g] = a.elapsed_time(b) / steps
     del grads, X, G, gbar, params, xc
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_reduce_easgd(tc, wl, w, sizes, g, steps, warmup):
+    """The AVG reduction and the step on both layouts, as two calls
+    (tc_reduce + easgd_step) and as one (reduce_easgd_step); average times
+    (ms) from HIP events on the stream, over `steps` back-to-back pairs or
+    calls."""
+    import torch
+
+    N, K = g.numel, w.K
+    dev = "cuda"
+    print(f"# setup reduction fused with the step: N={N} K={K}", file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream()
+    gs = wl.make_gradients(w, N, dev)
+    xs, xc = wl.make_state(w, N, dev)
+    gbar = torch.empty(N, dtype=torch.float32, device=dev)
+    X = torch.empty(tc.tensor_numel(g, K), dtype=torch.float32, device=dev)
+    G = torch.empty(tc.tensor_numel(g, K), dtype=gs[0].dtype, device=dev)
+    tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in xs]), X)
+    tc.pack_tensor(tc.TensorList(g, [wl.split_views(t, sizes) for t in gs]), G)
+    calls = {
+        "separate": (lambda: (tc.reduce(g, gs, gbar, "avg", stream),
+                              tc.easgd_step(g, xs, gs, xc, w.eta, w.rho, stream)),
+                     lambda: tc.reduce_easgd_step(g, xs, gs, xc, gbar, w.eta, w.rho, "avg", stream)),
+        "tensor": (lambda: (tc.reduce_tensor(g, K, G, gbar, "avg", stream),
+                            tc.easgd_step_tensor(g, K, X, G, xc, w.eta, w.rho, stream)),
+                   lambda: tc.reduce_easgd_step_tensor(g, K, X, G, xc, gbar, w.eta, w.rho, "avg", stream)),
+    }
+    out = {}
+    for lay, fns in calls.items():
+        out[lay] = []
+        for fn in fns:
+            for _ in range(warmup):
+                fn()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record(stream)
+            for _ in range(steps):
+                fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            out[lay].append(a.elapsed_time(b) / steps)
+    del gs, xs, xc, gbar, X, G
     torch.cuda.empty_cache()
     return out
 
@@ -579,6 +636,11 @@ def config_table(tc, wl, reps=20):
             nb = op_bytes("easgd", K, N, s_g)
             r["easgd separate"] = row(nb, [lambda: tc.easgd_step(g, xs, gsep[0], xc, w.eta, w.rho)])
             r["easgd tensor"] = row(nb, [lambda: tc.easgd_step_tensor(g, K, X, gten[0], xc2, w.eta, w.rho)])
+            nb = op_bytes("reduce_easgd", K, N, s_g)
+            r["reduce_avg + easgd, one call, separate"] = row(
+                nb, [lambda: tc.reduce_easgd_step(g, xs, gsep[0], xc, avg, w.eta, w.rho, "avg")])
+            r["reduce_avg + easgd, one call, tensor"] = row(
+                nb, [lambda: tc.reduce_easgd_step_tensor(g, K, X, gten[0], xc2, avg, w.eta, w.rho, "avg")])
             if "pack" in w.ops:
                 grads = tc.TensorList(g, layer_lists(tc, g, gsep[0], sizes))
                 params = tc.TensorList(g, [[torch.empty(n, device=dev) for n in sizes] for _ in range(K)])
@@ -674,7 +736,8 @@ def main():
     ap.add_argument("--no-compare", action="store_true", help="skip the other layout")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-fused", action="store_true",
-                    help="skip timing the one-pass pipeline (easgd_pipeline_tensor)")
+                    help="skip timing the one-pass pipeline (easgd_pipeline_tensor) and the reduction "
+                         "fused with the step (reduce_easgd_step)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip timing every configured workload's operations")
     ap.add_argument("--no-next-rows", action="store_true",
@@ -731,7 +794,8 @@ def main():
         return out
 
     kernels = kernel_table(per_op_ms)
-    dom = "easgd" if "easgd" in ops else max(ops, key=lambda o: per_op_ms[o])
+    dom = next((o for o in ("easgd", "reduce_easgd") if o in ops), None)
+    dom = dom or max(ops, key=lambda o: per_op_ms[o])
     traffic = recorded_traffic(args.workload, first).get(dom)
     roof = {"bound": "hbm", "kernel": f"{dom} ({first} layout)", "achieved": kernels[dom]["GB/s"],
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels[dom]["frac"], "traffic": traffic,
@@ -759,6 +823,19 @@ def main():
                           "speedup_vs_four_calls": round(four_ms / ft[write_g], 3),
                           "traffic": recorded_traffic(args.workload, "tensor").get(
                               "pipeline" if write_g else "pipeline_no_g")}
+
+    fused_re = None
+    if not args.no_fused and {"reduce", "easgd"} <= set(ops):
+        rt = run_reduce_easgd(tc, wl, w, sizes, g, args.steps, args.warmup)
+        b = op_bytes("reduce_easgd", K, N, s_g)
+        fused_re = {"entry_points": {"separate": "reduce_easgd_step", "tensor": "reduce_easgd_step_tensor"},
+                    "op": "avg", "algorithmic_bytes": b}
+        for lay, (two_ms, one_ms) in rt.items():
+            gbs = b / (one_ms * 1e-3) / 1e9
+            fused_re[lay] = {"ms": round(one_ms, 5), "per_s": round(1e3 / one_ms, 1), "GB/s": round(gbs, 1),
+                             "frac": round(gbs / HBM_PEAK_GBS, 4), "two_calls_ms": round(two_ms, 5),
+                             "speedup_vs_two_calls": round(two_ms / one_ms, 3),
+                             "traffic": recorded_traffic(args.workload, lay).get("reduce_easgd")}
 
     configs = None
     if not args.no_configs:
@@ -798,6 +875,7 @@ def main():
         "layouts": layouts,
         "roofline": roof,
         "fused_pipeline": fused,
+        "fused_reduce_easgd": fused_re,
         "configs": configs,
         "next_rows": extra,
         "cpu_baseline": cpu,

@@ -23,6 +23,10 @@ def test_algorithmic_bytes_resnet50_k8():
     # bfloat16 gradients: two bytes each where gradients are read
     assert bench.op_bytes("reduce", 16, 10, 2) == (16 * 2 + 4) * 10
     assert bench.op_bytes("easgd", 16, 10, 2) == ((8 + 2) * 16 + 8) * 10
+    # the reduction fused with the step: the step's bytes plus the average written,
+    # the gradients read once (36 + 104 - 32 per element at K = 8)
+    assert bench.op_bytes("reduce_easgd", 8, N_R50, 4) == 108 * N_R50
+    assert bench.op_bytes("reduce_easgd", 16, 10, 2) == ((8 + 2) * 16 + 12) * 10
 
 
 def test_pipeline_bytes():
