@@ -302,6 +302,9 @@ __device__ __forceinline__ f4 shfl4(f4 v, int src) {
     return f4{__shfl(v.x, src, 64), __shfl(v.y, src, 64), __shfl(v.z, src, 64), __shfl(v.w, src, 64)};
 }
 
+#ifndef TC_TEA_RED_GATHER
+#define TC_TEA_RED_GATHER 1
+#endif
 // RED: the step fused with the reduction of the gradients it reads, by the
 // reduction kernel's own butterflies and quotient (bit for bit its result).
 template <int P, typename T, int U, typename I, bool RED>
@@ -333,6 +336,7 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
     }
     const f4 rho = f4(a.rho), neg_eta = f4(-a.eta), alpha = f4(a.a);
     f4 cn[U];
+    f4 rout = f4(0.0f);  // RED at P >= 16: lane m < WS gathers the output of the wave's slot m
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const I j = j0 + I(u) * SPW;
@@ -344,7 +348,15 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
         if (!kShare && j < nslot && i == 0) store_slot_pol<TC_TEA_C_STORE_AUX, I>(a.xc, j, cn[u]);
         if constexpr (RED) {
             // the gradients of lanes past K, and of slots past the end, are +0
-            if constexpr (P >= 4) {
+            if constexpr (kShare && TC_TEA_RED_GATHER) {
+                // the full butterfly (the same tree as the split one), then
+                // the slot groups' sums gathered like the center, so that the
+                // wave writes its WS slots of the output with one store
+                f4 r = group_sum4<P>(g[u]);
+                if (a.op == TC_AVG) r = div_k<P>(r, K);
+                const f4 t = shfl4(r, (lane % SPW) * P);
+                if (lane / SPW == u) rout = t;
+            } else if constexpr (P >= 4) {
                 float r = split_group_sum<P>(g[u], threadIdx.x);
                 if (a.op == TC_AVG) r = div_k<P>(r, K);
                 if (j < nslot && i < 4) store_elem_pol<TC_TRD_STORE_AUX, I>(a.out, j, comp_of_lane(i), r);
@@ -366,28 +378,35 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
         }
         if (lane < WS && jw + static_cast<I>(lane) < nslot)
             store_slot_pol<TC_TEA_C_STORE_AUX, I>(a.xc, jw + static_cast<I>(lane), out);
+        if constexpr (RED && TC_TEA_RED_GATHER)
+            if (lane < WS && jw + static_cast<I>(lane) < nslot)
+                store_slot_pol<TC_TRD_STORE_AUX, I>(a.out, jw + static_cast<I>(lane), rout);
     }
     if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot
         const int64_t e = 4 * a.nslot + threadIdx.x;
         if (e < a.n) {
             const float cv = a.xc[e];
-            float d[P], gt[P];
+            float d[P];
 #pragma unroll
             for (int q = 0; q < P; ++q) {
                 if (q < K) {
                     const int64_t idx = (a.nslot * K + q) * 4 + (e & 3);
                     const float xv = a.x[idx];
-                    gt[q] = load_elem(a.g, idx);
                     d[q] = xv - cv;
-                    a.x[idx] = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, d[q], gt[q]), xv);
+                    a.x[idx] = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, d[q], load_elem(a.g, idx)), xv);
                 } else {
                     d[q] = 0.0f;
-                    gt[q] = 0.0f;
                 }
             }
             a.xc[e] = __builtin_fmaf(a.a, Tree<P>::sum(d), cv);
             if constexpr (RED) {
-                float r = Tree<P>::sum(gt);
+                // the gradients again, once the center's terms are summed:
+                // holding both sets of P terms would size every lane of the
+                // kernel for them
+                float t[P];
+#pragma unroll
+                for (int q = 0; q < P; ++q) t[q] = q < K ? load_elem(a.g, (a.nslot * K + q) * 4 + (e & 3)) : 0.0f;
+                float r = Tree<P>::sum(t);
                 if (a.op == TC_AVG) r = div_k<P>(r, K);
                 a.out[e] = r;
             }

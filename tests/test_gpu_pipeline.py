@@ -414,8 +414,9 @@ def test_resnet50_k8_100_iterations_every_path(orc):
 def test_steps_replay_from_a_hip_graph(case):
     """Every data entry point only launches kernels (no allocation, no
     synchronisation, no memset), so a step can be captured in a HIP graph.
-    The four calls and the one-launch pipeline are captured once and
-    replayed five times, with eager work and synchronisations between the
+    The four calls, the three calls with the reduction and the step as one
+    (reduce_easgd_step_tensor), and the one-launch pipeline are captured once
+    and replayed five times, with eager work and synchronisations between the
     replays; after every replay the state equals the same number of eager
     steps, bit for bit.  The tiny group takes the straight paths; the
     second case (lengths not multiples of 4, bfloat16 gradient tensors one
@@ -454,10 +455,15 @@ def test_steps_replay_from_a_hip_graph(case):
         tc.easgd_step_tensor(g, K, st["X"], st["G"], st["c"], eta, rho, s)
         tc.unpack_tensor(st["ptl"], st["X"], s)
 
+    def three(st, s):
+        tc.pack_tensor(grads, st["G"], s)
+        tc.reduce_easgd_step_tensor(g, K, st["X"], st["G"], st["c"], st["gbar"], eta, rho, "avg", s)
+        tc.unpack_tensor(st["ptl"], st["X"], s)
+
     def one(st, s):
         tc.easgd_pipeline_tensor(grads, st["ptl"], st["G"], st["gbar"], st["X"], st["c"], eta, rho, s)
 
-    for step in (four, one):
+    for step in (four, three, one):
         eager, graphed = make(), make()
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
@@ -479,8 +485,10 @@ def test_steps_replay_from_a_hip_graph(case):
         del graph
 
 
-def test_separate_buffer_step_replays_from_a_hip_graph():
-    """The separate-buffer step (pack, AVG, fused step, unpack; the pointer
+@pytest.mark.parametrize("fused", [False, True])
+def test_separate_buffer_step_replays_from_a_hip_graph(fused):
+    """The separate-buffer step (pack, AVG, fused step, unpack; or pack, the
+    AVG and the step as one reduce_easgd_step call, unpack; the pointer
     arrays travel as launch arguments) captured once and replayed five times
     equals five eager steps bit for bit after every replay."""
     w = wl.WORKLOADS["tiny_k2"]
@@ -499,8 +507,11 @@ def test_separate_buffer_step_replays_from_a_hip_graph():
 
     def step(st, s):
         tc.pack(grads, st["g"], s)
-        tc.reduce(g, st["g"], st["gbar"], "avg", s)
-        tc.easgd_step(g, st["x"], st["g"], st["c"], w.eta, w.rho, s)
+        if fused:
+            tc.reduce_easgd_step(g, st["x"], st["g"], st["c"], st["gbar"], w.eta, w.rho, "avg", s)
+        else:
+            tc.reduce(g, st["g"], st["gbar"], "avg", s)
+            tc.easgd_step(g, st["x"], st["g"], st["c"], w.eta, w.rho, s)
         tc.unpack(st["ptl"], st["x"], s)
 
     eager, graphed = make(), make()
