@@ -29,6 +29,20 @@ def test_algorithmic_bytes_resnet50_k8():
     assert bench.op_bytes("reduce_easgd", 16, 10, 2) == ((8 + 2) * 16 + 12) * 10
 
 
+def test_every_bench_workload_has_byte_counts():
+    # each op a bench step may run has an algorithmic byte count; a step with
+    # the reduction and the step as one call moves the four-call step's bytes
+    # less the second read of the K gradients (K * s_g per element)
+    for name, (wkey, ops, layout) in bench.WORKLOADS.items():
+        w = wl.WORKLOADS[wkey]
+        s_g = 2 if w.g_dtype == "bf16" else 4
+        assert layout in bench.LAYOUTS, name
+        total = sum(bench.op_bytes(op, w.K, 1000, s_g) for op in ops)
+        if "reduce_easgd" in ops:
+            four = ("pack", "reduce", "easgd", "unpack")
+            assert total == sum(bench.op_bytes(op, w.K, 1000, s_g) for op in four) - w.K * s_g * 1000, name
+
+
 def test_pipeline_bytes():
     # read K gradient lists, K workers, the center; write the packed
     # gradients (optional), the AVG, K workers, the center, K parameter lists
