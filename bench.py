@@ -132,6 +132,10 @@ def recorded_traffic(workload: str, layout: str):
     WRITE_SIZE summary of this workload and layout, or {} when there is none
     or the kernels have changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", f"{workload}_{layout}_hbm_traffic.md")
+    if not os.path.exists(path) and workload.endswith("_fused"):
+        # the same group and kernels as the four-call workload, whose counter
+        # passes include the fused call
+        path = os.path.join(ROOT, "profiles", f"{workload[:-len('_fused')]}_pipeline_{layout}_hbm_traffic.md")
     if not os.path.exists(path):
         return {}
     vals = {}
