@@ -767,6 +767,9 @@ __device__ __forceinline__ void load_windows(const uintptr_t (&S)[N], u4 (&out)[
 #ifndef TC_TPACK_GROUP_BYTES
 #define TC_TPACK_GROUP_BYTES 128
 #endif
+#ifndef TC_TPACK_GROUP_WHOLE
+#define TC_TPACK_GROUP_WHOLE 1
+#endif
 // The direct binary32 pack and unpack are compiled for at least 4 waves per
 // SIMD (amdgpu_waves_per_eu; they already run at 6, so the hint takes no
 // occupancy): measured on MI355X, VGG-16 at K = 4 packs 3% and unpacks 2%
@@ -1575,6 +1578,9 @@ hipError_t launch_tensor_easgd(int K, float* x, const void* g, int g_dtype, floa
     return dispatch_teasgd<float>(K, x, g, xc, out, op, eta, rho, n, stream);
 }
 
+#ifndef TC_TPACK_FINE_K
+#define TC_TPACK_FINE_K 12
+#endif
 template <int P, bool DIRECT>
 hipError_t run_tpack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStream_t stream) {
     const tc_group* g = tl->g;
@@ -1586,15 +1592,23 @@ hipError_t run_tpack(const tc_tensorlist* tl, void* tensor, bool unpack, hipStre
     //   unpack 12-57% in bfloat16 and 20-35% for misaligned lists), except
     //   the direct binary32 unpack at P = 2 (1-3% slower with them), and
     //   groups too small to fill the chip with them (kMinLongerChunks);
-    // - unpack through the tiles, on a group of large tensors, takes the
-    //   shorter chunking when a tile fits in its chunks (P >= 8; at P = 4
-    //   the tiles would leave half the lanes idle).
+    // - through the tiles, where a tile fits in its chunks (P >= 8; at P = 4
+    //   the tiles would leave half the lanes idle), the shorter chunking
+    //   (TC_TPACK_CHUNK_FINE) serves unpack on a group of large tensors or
+    //   with the copies taken in groups, and pack from K = TC_TPACK_FINE_K.
+    //   Measured on MI355X against TC_TPACK_CHUNK: pack +2.5-5.5% at K = 12
+    //   to 31 on ResNet-50 (3-6.6% slower at K = 9), +3% on the 10,000-tensor
+    //   group at K = 16; its binary32 unpack +5% at K = 16 (copy groups) but
+    //   6.5% slower at K = 12 (no groups).
     constexpr int fine_slots = TC_TPACK_CHUNK_FINE / 4;
-    const bool fits = tl->elem == 2 ? tpack_tile_slots<P, 2, true>() <= fine_slots
-                                    : tpack_tile_slots<P, 4, true>() <= fine_slots;
+    const int tile = unpack ? (tl->elem == 2 ? tpack_tile_slots<P, 2, true>() : tpack_tile_slots<P, 4, true>())
+                            : (tl->elem == 2 ? tpack_tile_slots<P, 2, false>() : tpack_tile_slots<P, 4, false>());
+    const bool fits = tile <= fine_slots;
     const bool longer =
         P <= 2 && !(DIRECT && unpack && tl->elem == 4 && P == 2) && g->sep.nchunks >= kMinLongerChunks;
-    const tc_chunking& c = longer ? g->sep : unpack && !DIRECT && g->large && fits ? g->tpack_fine : g->tpack;
+    const bool grouped = P < next_pow2(tl->K);
+    const bool fine = !DIRECT && fits && (unpack ? g->large || grouped : tl->K >= TC_TPACK_FINE_K);
+    const tc_chunking& c = longer ? g->sep : fine ? g->tpack_fine : g->tpack;
     const int groups = (tl->K + P - 1) / P;
     TPackArgs a{g->d_offsets, c.d_first, tl->d_ptrs, tensor, g->n, tl->K, g->N, c.chunk, groups};
     dim3 grid(static_cast<unsigned>(c.nchunks * groups));
@@ -1628,10 +1642,14 @@ hipError_t launch_tensor_pack(const tc_tensorlist* tl, void* tensor, bool unpack
     // 10,000-tensor group's binary32 unpack +12% at K = 16 and +6.5% at
     // K = 32 (its bfloat16 pack +2% at K = 32), ResNet-50 and VGG-16 at K =
     // 16 and 32 level to +3%; at K = 64 up to 4% slower, and groups of 64
-    // bytes (half lines) 11-33% slower everywhere.
+    // bytes (half lines) 11-33% slower everywhere.  Only when the groups are
+    // whole (TC_TPACK_GROUP_WHOLE: K a multiple of the group size): a last,
+    // partial group writes pieces of every slot row that fill no line, and
+    // leaves most of its lanes idle.  With it, ResNet-50 at K = 9 to 15 and
+    // 31 packed at 2.0-2.2 TB/s; in one group, 5.3-5.9 (unpack +20-38%).
     const int pg = TC_TPACK_GROUP_BYTES / (4 * tl->elem);
     const int pk = next_pow2(tl->K);
-    const int pt = !direct && pg > 0 && pk > pg && pk <= 32 ? pg : pk;
+    const int pt = !direct && pg > 0 && pk > pg && pk <= 32 && (!TC_TPACK_GROUP_WHOLE || tl->K % pg == 0) ? pg : pk;
     switch (pt) {
 #define TC_CASE(p) \
     case p: return direct ? run_tpack<p, true>(tl, tensor, unpack, stream) \
