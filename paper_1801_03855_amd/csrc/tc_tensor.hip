@@ -305,6 +305,9 @@ __device__ __forceinline__ f4 shfl4(f4 v, int src) {
 #ifndef TC_TEA_RED_GATHER
 #define TC_TEA_RED_GATHER 1
 #endif
+#ifndef TC_TEA_RED_SPLIT
+#define TC_TEA_RED_SPLIT 1
+#endif
 // RED: the step fused with the reduction of the gradients it reads, by the
 // reduction kernel's own butterflies and quotient (bit for bit its result).
 template <int P, typename T, int U, typename I, bool RED>
@@ -349,12 +352,20 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
         if constexpr (RED) {
             // the gradients of lanes past K, and of slots past the end, are +0
             if constexpr (kShare && TC_TEA_RED_GATHER) {
-                // the full butterfly (the same tree as the split one), then
                 // the slot groups' sums gathered like the center, so that the
-                // wave writes its WS slots of the output with one store
-                f4 r = group_sum4<P>(g[u]);
-                if (a.op == TC_AVG) r = div_k<P>(r, K);
-                const f4 t = shfl4(r, (lane % SPW) * P);
+                // wave writes its WS slots of the output with one store, and
+                // the AVG quotient taken once, after the gather.  The split
+                // butterfly leaves lane c' of a slot group with component
+                // comp_of_lane(c') (a self-inverse map of its two low bits);
+                // the gather reads the four components from those lanes.
+#if TC_TEA_RED_SPLIT
+                const float r1 = split_group_sum<P>(g[u], threadIdx.x);
+                const int base = (lane % SPW) * P;
+                const f4 t{__shfl(r1, base, 64), __shfl(r1, base + 2, 64), __shfl(r1, base + 1, 64),
+                           __shfl(r1, base + 3, 64)};
+#else
+                const f4 t = shfl4(group_sum4<P>(g[u]), (lane % SPW) * P);
+#endif
                 if (lane / SPW == u) rout = t;
             } else if constexpr (P >= 4) {
                 float r = split_group_sum<P>(g[u], threadIdx.x);
@@ -378,9 +389,11 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
         }
         if (lane < WS && jw + static_cast<I>(lane) < nslot)
             store_slot_pol<TC_TEA_C_STORE_AUX, I>(a.xc, jw + static_cast<I>(lane), out);
-        if constexpr (RED && TC_TEA_RED_GATHER)
+        if constexpr (RED && TC_TEA_RED_GATHER) {
+            if (a.op == TC_AVG) rout = div_k<P>(rout, K);
             if (lane < WS && jw + static_cast<I>(lane) < nslot)
                 store_slot_pol<TC_TRD_STORE_AUX, I>(a.out, jw + static_cast<I>(lane), rout);
+        }
     }
     if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot
         const int64_t e = 4 * a.nslot + threadIdx.x;
