@@ -615,6 +615,13 @@ __global__ __launch_bounds__(256) void tensor_async_kernel(TStepArgs<float> a) {
 #ifndef TC_TBCAST_UNROLL
 #define TC_TBCAST_UNROLL 2
 #endif
+// K not a power of two takes tensor_bcast_dense_kernel.  Measured on MI355X
+// against the slot-group mapping, sources rotated (ResNet-50 group): K = 3
+// to 12 +5.5-18%, K = 17 and 33 +31-34% (4.0-4.1 -> 5.3 TB/s), K = 20 to 48
+// +8-18%, bfloat16 K = 17 and 33 +50%.
+#ifndef TC_TBCAST_DENSE
+#define TC_TBCAST_DENSE 1
+#endif
 template <int P, typename T, int U, typename I>
 __global__ __launch_bounds__(256) void tensor_bcast_kernel(const T* src, T* dst, int64_t nslot, int64_t n, int K) {
     constexpr int SB = 4 * sizeof(T);
@@ -634,6 +641,36 @@ __global__ __launch_bounds__(256) void tensor_bcast_kernel(const T* src, T* dst,
         const I j = j0 + I(u) * SPW;
         if (j < ns && i < K)
             __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(reinterpret_cast<char*>(dst) + (j * I(K) + I(i)) * I(SB)));
+    }
+    if (blockIdx.x == gridDim.x - 1) {
+        const int64_t e = 4 * nslot + threadIdx.x;
+        if (e < n)
+            for (int q = 0; q < K; ++q) dst[(nslot * K + q) * 4 + (e & 3)] = src[e];
+    }
+}
+
+// The same broadcast with every lane busy when K is not a power of two: the
+// destination's whole slots are nslot * K consecutive pieces, lane by lane
+// (piece p holds slot p / K of the source), so a wave writes 64 pieces
+// whatever K is, where the slot-group mapping leaves P - K of every P lanes
+// idle.  A workgroup takes U passes of 256 consecutive pieces.
+template <typename T, int U, typename I>
+__global__ __launch_bounds__(256) void tensor_bcast_dense_kernel(const T* src, T* dst, int64_t nslot, int64_t n,
+                                                                 int K) {
+    constexpr int SB = 4 * sizeof(T);
+    using V = typename std::conditional<SB == 16, u4, u2>::type;
+    const I np = static_cast<I>(nslot) * static_cast<I>(K);
+    const I p0 = static_cast<I>(tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x)) * I(256 * U) + threadIdx.x;
+    V v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const I p = p0 + I(u * 256);
+        if (p < np) v[u] = *reinterpret_cast<const V*>(reinterpret_cast<const char*>(src) + (p / I(K)) * I(SB));
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const I p = p0 + I(u * 256);
+        if (p < np) __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(reinterpret_cast<char*>(dst) + p * I(SB)));
     }
     if (blockIdx.x == gridDim.x - 1) {
         const int64_t e = 4 * nslot + threadIdx.x;
@@ -1819,6 +1856,17 @@ hipError_t run_tbcast(const void* src, void* dst, int K, int64_t n, hipStream_t 
     constexpr int U = TC_TBCAST_UNROLL;
     constexpr int SPB = 256 / P;
     const int64_t nslot = n / 4;
+    if (TC_TBCAST_DENSE && K != P) {
+        const int64_t blocks = (nslot * K + 256 * U - 1) / (256 * U);
+        dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+        if ((nslot + 1) * K * 16 < (int64_t(1) << 32))
+            hipLaunchKernelGGL((tensor_bcast_dense_kernel<T, U, uint32_t>), grid, dim3(256), 0, s,
+                               static_cast<const T*>(src), static_cast<T*>(dst), nslot, n, K);
+        else
+            hipLaunchKernelGGL((tensor_bcast_dense_kernel<T, U, int64_t>), grid, dim3(256), 0, s,
+                               static_cast<const T*>(src), static_cast<T*>(dst), nslot, n, K);
+        return hipGetLastError();
+    }
     const int64_t blocks = (nslot + SPB * U - 1) / (SPB * U);
     dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
     if ((nslot + 1) * K * 16 < (int64_t(1) << 32))
