@@ -25,11 +25,12 @@ namespace tc {
 //   elements (the bytes of a binary32 chunk);
 // - tensor-layout pack/unpack, whose workgroups move all K copies of a chunk:
 //   1,024 elements (against 2,048 and 512 on VGG-16's straight path, and
-//   against 512 and 2,048 to 8,192 on 10,000 small tensors), but 512 for
-//   the unpack through the tiles on groups of large tensors (ResNet-50:
-//   4-5% faster at K = 8, 8% at K = 16; the pack is 3% slower there), and
-//   the separate-buffer chunks at P <= 2 (except the direct binary32
-//   unpack at P = 2), where 1,024 elements move only 4-16 KB;
+//   against 512 and 2,048 to 8,192 on 10,000 small tensors), but 512
+//   through the tiles for the unpack on groups of large tensors (ResNet-50:
+//   4-5% faster at K = 8, 8% at K = 16) or with copy groups, and for the
+//   pack from K = 12 (at K <= 8 it is 3-9% slower), and the separate-buffer
+//   chunks at P <= 2 (except the direct binary32 unpack at P = 2), where
+//   1,024 elements move only 4-16 KB;
 // - the pipelined step: 512 elements (7-8% faster than 2,048 on ResNet-50,
 //   VGG-16 and 10,000 small tensors; 2% faster than 1,024 on the latter),
 //   but the tensor-layout pack's 1,024 at P = 1, and at P = 2 except for
@@ -191,7 +192,7 @@ struct tc_group {
     bool large = false;            // mean tensor size >= TC_PACK_LARGE_MEAN
     tc_chunking sep;               // separate-buffer pack/unpack
     tc_chunking tpack;             // tensor-layout pack/unpack
-    tc_chunking tpack_fine;        // unpack through the tiles, large tensors
+    tc_chunking tpack_fine;        // tensor-layout pack/unpack through the tiles, where shorter chunks pay
     tc_chunking pipe;              // the pipelined step
     tc_chunking sep2;              // separate-buffer pack/unpack, 2-byte elements
     bool slot_bounds = false;      // every tensor boundary before the last,
