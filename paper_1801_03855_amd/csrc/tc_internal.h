@@ -25,12 +25,11 @@ namespace tc {
 //   elements (the bytes of a binary32 chunk);
 // - tensor-layout pack/unpack, whose workgroups move all K copies of a chunk:
 //   1,024 elements (against 2,048 and 512 on VGG-16's straight path, and
-//   against 512 and 2,048 to 8,192 on 10,000 small tensors), but 512
-//   through the tiles for the unpack on groups of large tensors (ResNet-50:
-//   4-5% faster at K = 8, 8% at K = 16) or with copy groups, and for the
-//   pack from K = 12 (at K <= 8 it is 3-9% slower), and the separate-buffer
-//   chunks at P <= 2 (except the direct binary32 unpack at P = 2), where
-//   1,024 elements move only 4-16 KB;
+//   against 512 and 2,048 to 8,192 on 10,000 small tensors), but 512 through
+//   the tiles for unpack on large-tensor groups (ResNet-50 K = 8 +4-5%) or
+//   with copy groups, and for pack from K = 12 (3-9% slower at K <= 8); and
+//   the separate-buffer chunks at P <= 2 (but the direct binary32 unpack at
+//   P = 2), where 1,024 elements move only 4-16 KB;
 // - the pipelined step: 512 elements (7-8% faster than 2,048 on ResNet-50,
 //   VGG-16 and 10,000 small tensors; 2% faster than 1,024 on the latter),
 //   but the tensor-layout pack's 1,024 at P = 1, and at P = 2 except for
