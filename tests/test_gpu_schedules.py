@@ -248,9 +248,10 @@ def test_period_schedule_matches_oracle(orc, layout):
 # with a partial last workgroup whose lanes past the end repeat the last
 # slot and a ragged tail; (4, 4099): one copy group of four.  (17, 4099),
 # (33, 100001): K just above a power of two, where the tensor layout's
-# broadcast maps lanes to pieces densely.
+# broadcast maps lanes to pieces densely; (3, 2): that mapping with no whole
+# slot, the element tail alone.
 @pytest.mark.parametrize("K,N", [(1, 7), (3, 4097), (8, 100003), (16, 5), (5, 17000003), (1, 4), (1, 1000003),
-                                 (4, 4099), (17, 4099), (33, 100001)])
+                                 (4, 4099), (17, 4099), (33, 100001), (3, 2)])
 def test_broadcast(orc, layout, dtype, K, N):
     g = tc.Group([N])
     src = torch.randn(N, device=DEV).to(dtype)
