@@ -89,6 +89,7 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
     g->tpack.chunk = TC_TPACK_CHUNK;
     g->tpack_fine.chunk = TC_TPACK_CHUNK_FINE;
     g->pipe.chunk = TC_PIPE_CHUNK;
+    g->pipe_fine.chunk = TC_PIPE_CHUNK_FINE;
     // 2-byte elements on groups of large tensors: chunks of twice the
     // elements, the bytes of a binary32 chunk (measured on MI355X, bfloat16
     // pack and unpack on ResNet-50 at K = 2-16 and VGG-16 at K = 4: 13-17%
@@ -103,7 +104,7 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         auto it = std::upper_bound(g->offsets.begin(), g->offsets.begin() + n, j);
         return static_cast<int32_t>(it - g->offsets.begin()) - 1;
     };
-    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe, &g->sep2}) {
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe, &g->pipe_fine, &g->sep2}) {
         c->nchunks = (g->N + c->chunk - 1) / c->chunk;
         if (c->nchunks > INT32_MAX / 2) { set_error("group too large"); delete g; return nullptr; }
         c->first.resize(static_cast<size_t>(c->nchunks) + 1);
@@ -123,7 +124,7 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
         tc_group_destroy(g);
         return nullptr;
     }
-    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe, &g->sep2}) {
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe, &g->pipe_fine, &g->sep2}) {
         const size_t cb = c->first.size() * sizeof(int32_t);
         if ((e = hipMalloc(&c->d_first, cb)) != hipSuccess ||
             (e = hipMemcpy(c->d_first, c->first.data(), cb, hipMemcpyHostToDevice)) != hipSuccess) {
@@ -138,7 +139,7 @@ TC_API tc_group* tc_group_create(const int64_t* sizes, int32_t n) {
 TC_API void tc_group_destroy(tc_group* g) {
     if (!g) return;
     if (g->d_offsets) (void)hipFree(g->d_offsets);
-    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe, &g->sep2})
+    for (tc_chunking* c : {&g->sep, &g->tpack, &g->tpack_fine, &g->pipe, &g->pipe_fine, &g->sep2})
         if (c->d_first) (void)hipFree(c->d_first);
     delete g;
 }

@@ -33,7 +33,8 @@ namespace tc {
 // - the pipelined step: 512 elements (7-8% faster than 2,048 on ResNet-50,
 //   VGG-16 and 10,000 small tensors; 2% faster than 1,024 on the latter),
 //   but the tensor-layout pack's 1,024 at P = 1, and at P = 2 except for
-//   binary32 gradients on the straight path.
+//   binary32 gradients on the straight path, and 256 on groups of large
+//   tensors from K = 8 (+2.5-7% there).
 // All are multiples of every vector width (4, 8).
 #ifndef TC_PACK_CHUNK_LARGE
 #define TC_PACK_CHUNK_LARGE 2048
@@ -49,6 +50,9 @@ namespace tc {
 #endif
 #ifndef TC_PIPE_CHUNK
 #define TC_PIPE_CHUNK 512
+#endif
+#ifndef TC_PIPE_CHUNK_FINE
+#define TC_PIPE_CHUNK_FINE 256
 #endif
 #ifndef TC_PACK_LARGE_MEAN
 #define TC_PACK_LARGE_MEAN 32768
@@ -193,6 +197,7 @@ struct tc_group {
     tc_chunking tpack;             // tensor-layout pack/unpack
     tc_chunking tpack_fine;        // tensor-layout pack/unpack through the tiles, where shorter chunks pay
     tc_chunking pipe;              // the pipelined step
+    tc_chunking pipe_fine;         // the pipelined step, shorter chunks
     tc_chunking sep2;              // separate-buffer pack/unpack, 2-byte elements
     bool slot_bounds = false;      // every tensor boundary before the last,
                                    // partial slot is a multiple of 4

@@ -1741,10 +1741,21 @@ constexpr bool pipe_direct_pays() { return (64 / P) * 4 * static_cast<int>(sizeo
 // faster; the straight binary32 path at K = 2 6% faster on ResNet-50 but 9%
 // slower on VGG-16; at P = 4 the longer chunks lost 4-8%, and the separate-
 // buffer pack's chunks (2,048 or 4,096 elements) gained less at P <= 2.
+// On groups of large tensors from K = TC_PIPE_FINE_K, chunks of
+// TC_PIPE_CHUNK_FINE elements: each workgroup then moves half the bytes, and
+// those resident at one time cover a smaller window of the buffers.
+// Measured on MI355X against 512 elements: ResNet-50 K = 8 +2.5%, K = 16 to
+// 64 +1.3-2.6%, VGG-16 K = 8 and 16 +2-3%, bfloat16 gradients at K = 8 and
+// 16 +5.7-7.3%; at K = 5 2% slower, and on the 10,000-tensor group 3-4%
+// slower at K = 16.
+#ifndef TC_PIPE_FINE_K
+#define TC_PIPE_FINE_K 8
+#endif
 template <int P, typename T>
 hipError_t run_tpipe(const tc_group* g, TPipeArgs a, bool direct, hipStream_t stream) {
     const bool longer = (P == 1 || (P == 2 && !(direct && sizeof(T) == 4))) && g->tpack.nchunks >= kMinLongerChunks;
-    const tc_chunking& c = longer ? g->tpack : g->pipe;
+    const bool fine = !longer && TC_PIPE_FINE_K > 0 && g->large && a.K >= TC_PIPE_FINE_K;
+    const tc_chunking& c = longer ? g->tpack : fine ? g->pipe_fine : g->pipe;
     a.chunk_first = c.d_first;
     a.chunk = c.chunk;
     const unsigned blocks = static_cast<unsigned>(c.nchunks);

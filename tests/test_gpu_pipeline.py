@@ -220,6 +220,17 @@ def test_longer_chunks(orc, K, gdt, misalign):
     _run(orc, sizes, K, gdt=gdt, seed=120 + K, misalign=misalign)
 
 
+@pytest.mark.parametrize("K,gdt,misalign", [(5, torch.float32, False), (8, torch.float32, False),
+                                            (8, torch.bfloat16, True), (16, torch.float32, True),
+                                            (33, torch.bfloat16, False)])
+def test_large_tensor_groups(orc, K, gdt, misalign):
+    """A group of large tensors (2.2M elements in three tensors) at K >= 5,
+    on the straight path (slot-aligned, binary32 up to K = 8) and through
+    the tiles, with the chunking such groups take at these K."""
+    sizes = [700_000, 900_004, 600_000, 7] if not misalign else [700_001, 900_003, 600_002, 7]
+    _run(orc, sizes, K, gdt=gdt, seed=140 + K, misalign=misalign)
+
+
 @pytest.mark.parametrize("gdt", [torch.float32, torch.bfloat16])
 def test_slot_sizes_misaligned_pointers(orc, gdt):
     """Slot-multiple sizes but tensors one element into their allocations:
