@@ -654,23 +654,47 @@ __global__ __launch_bounds__(256) void tensor_bcast_kernel(const T* src, T* dst,
 // (piece p holds slot p / K of the source), so a wave writes 64 pieces
 // whatever K is, where the slot-group mapping leaves P - K of every P lanes
 // idle.  A workgroup takes U passes of 256 consecutive pieces.
-template <typename T, int U, typename I>
+template <typename T, int U, int PPL, typename I>
 __global__ __launch_bounds__(256) void tensor_bcast_dense_kernel(const T* src, T* dst, int64_t nslot, int64_t n,
                                                                  int K) {
     constexpr int SB = 4 * sizeof(T);
     using V = typename std::conditional<SB == 16, u4, u2>::type;
     const I np = static_cast<I>(nslot) * static_cast<I>(K);
     const I p0 = static_cast<I>(tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x)) * I(256 * U) + threadIdx.x;
-    V v[U];
+    const char* sp = reinterpret_cast<const char*>(src);
+    char* dp = reinterpret_cast<char*>(dst);
+    if constexpr (PPL == 1) {
+        V v[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const I p = p0 + I(u * 256);
-        if (p < np) v[u] = *reinterpret_cast<const V*>(reinterpret_cast<const char*>(src) + (p / I(K)) * I(SB));
-    }
+        for (int u = 0; u < U; ++u) {
+            const I p = p0 + I(u * 256);
+            if (p < np) v[u] = *reinterpret_cast<const V*>(sp + (p / I(K)) * I(SB));
+        }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const I p = p0 + I(u * 256);
-        if (p < np) __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(reinterpret_cast<char*>(dst) + p * I(SB)));
+        for (int u = 0; u < U; ++u) {
+            const I p = p0 + I(u * 256);
+            if (p < np) __builtin_nontemporal_store(v[u], reinterpret_cast<V*>(dp + p * I(SB)));
+        }
+    } else {
+        // 8-byte pieces two to a lane (pieces 2q and 2q + 1), stored as one
+        // 16-byte granule (the buffer is 16-byte aligned)
+        static_assert(SB == 8 && PPL == 2, "two pieces a lane are for 8-byte pieces");
+        u2 v[U][2];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const I q = 2 * (p0 + I(u * 256));
+            if (q < np) v[u][0] = *reinterpret_cast<const u2*>(sp + (q / I(K)) * I(SB));
+            if (q + 1 < np) v[u][1] = *reinterpret_cast<const u2*>(sp + ((q + 1) / I(K)) * I(SB));
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const I q = 2 * (p0 + I(u * 256));
+            if (q + 1 < np)
+                __builtin_nontemporal_store(u4{v[u][0].x, v[u][0].y, v[u][1].x, v[u][1].y},
+                                            reinterpret_cast<u4*>(dp + q * I(SB)));
+            else if (q < np)
+                __builtin_nontemporal_store(v[u][0], reinterpret_cast<u2*>(dp + q * I(SB)));
+        }
     }
     if (blockIdx.x == gridDim.x - 1) {
         const int64_t e = 4 * nslot + threadIdx.x;
@@ -1793,8 +1817,44 @@ hipError_t launch_tensor_pipeline(const tc_tensorlist* grads, const tc_tensorlis
 #ifndef TC_TASYNC_U
 #define TC_TASYNC_U 2
 #endif
+// Plain SGD on the tensor layout is elementwise over the whole buffer: when K
+// is not a power of two, lanes take its pieces one after another (as the
+// dense broadcast does), so no lane of a slot group idles.  The arithmetic
+// per piece is the slot kernel's.
+template <typename T, typename I>
+__global__ __launch_bounds__(256) void tensor_sgd_dense_kernel(TStepArgs<T> a) {
+    const I np = static_cast<I>(a.nslot) * static_cast<I>(a.K);
+    const I p = static_cast<I>(tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x)) * I(256) + threadIdx.x;
+    if (p < np) {
+        const f4 x = load_slot(a.x, p), g = load_slot(static_cast<const T*>(a.g), p);
+        store_slot(a.x, p, fma4(f4(-a.s0), g, x));
+    }
+    if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot, element by element
+        const int64_t e = 4 * a.nslot + threadIdx.x;
+        if (e < a.n)
+            for (int q = 0; q < a.K; ++q) {
+                const int64_t k = (a.nslot * a.K + q) * 4 + (e & 3);
+                a.x[k] = __builtin_fmaf(-a.s0, load_elem(static_cast<const T*>(a.g), k), a.x[k]);
+            }
+    }
+}
+
+#ifndef TC_TSGD_DENSE
+#define TC_TSGD_DENSE 1
+#endif
 template <TOp OP, int P, typename T>
 hipError_t run_tstep(const TStepArgs<T>& a, hipStream_t s) {
+    if constexpr (OP == TOp::Sgd) {
+        if (TC_TSGD_DENSE && a.K != P) {
+            const int64_t blocks = (a.nslot * a.K + 255) / 256;
+            dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+            if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
+                hipLaunchKernelGGL((tensor_sgd_dense_kernel<T, uint32_t>), grid, dim3(256), 0, s, a);
+            else
+                hipLaunchKernelGGL((tensor_sgd_dense_kernel<T, int64_t>), grid, dim3(256), 0, s, a);
+            return hipGetLastError();
+        }
+    }
     if constexpr (OP == TOp::Async && P >= 4 && sizeof(T) == 4) {
         constexpr int U = TC_TASYNC_U;
         constexpr int SPB = 256 / P * U;
@@ -1862,21 +1922,31 @@ hipError_t launch_tensor_elastic_async(int K, float* x, float* xc, const int32_t
     return tstep<TOp::Async>(K, x, nullptr, TC_F32, xc, alpha, 0, order, R, n, s);
 }
 
+template <typename T, int U, int PPL>
+hipError_t run_tbcast_dense(const void* src, void* dst, int K, int64_t nslot, int64_t n, hipStream_t s) {
+    const int64_t blocks = (nslot * K + 256 * U * PPL - 1) / (256 * U * PPL);
+    dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+    if ((nslot + 1) * K * 16 < (int64_t(1) << 32))
+        hipLaunchKernelGGL((tensor_bcast_dense_kernel<T, U, PPL, uint32_t>), grid, dim3(256), 0, s,
+                           static_cast<const T*>(src), static_cast<T*>(dst), nslot, n, K);
+    else
+        hipLaunchKernelGGL((tensor_bcast_dense_kernel<T, U, PPL, int64_t>), grid, dim3(256), 0, s,
+                           static_cast<const T*>(src), static_cast<T*>(dst), nslot, n, K);
+    return hipGetLastError();
+}
+
 template <int P, typename T>
 hipError_t run_tbcast(const void* src, void* dst, int K, int64_t n, hipStream_t s) {
     constexpr int U = TC_TBCAST_UNROLL;
     constexpr int SPB = 256 / P;
     const int64_t nslot = n / 4;
     if (TC_TBCAST_DENSE && K != P) {
-        const int64_t blocks = (nslot * K + 256 * U - 1) / (256 * U);
-        dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
-        if ((nslot + 1) * K * 16 < (int64_t(1) << 32))
-            hipLaunchKernelGGL((tensor_bcast_dense_kernel<T, U, uint32_t>), grid, dim3(256), 0, s,
-                               static_cast<const T*>(src), static_cast<T*>(dst), nslot, n, K);
-        else
-            hipLaunchKernelGGL((tensor_bcast_dense_kernel<T, U, int64_t>), grid, dim3(256), 0, s,
-                               static_cast<const T*>(src), static_cast<T*>(dst), nslot, n, K);
-        return hipGetLastError();
+        // 8-byte (bf16) pieces go two to a lane from K = 33 on, one to a lane
+        // below that: measured on MI355X, two a lane was 10-13% faster at
+        // K = 33 and 48 and 3-6% slower at K = 3 to 20
+        if constexpr (sizeof(T) == 2)
+            if (K > 32) return run_tbcast_dense<T, U, 2>(src, dst, K, nslot, n, s);
+        return run_tbcast_dense<T, U, 1>(src, dst, K, nslot, n, s);
     }
     const int64_t blocks = (nslot + SPB * U - 1) / (SPB * U);
     dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));

@@ -65,10 +65,15 @@ LAYOUTS = ["separate", "tensor"]
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
-@pytest.mark.parametrize("K,gdt", [(1, torch.float32), (3, torch.float32), (8, torch.bfloat16),
-                                   (16, torch.float32), (33, torch.float32)])
-def test_sgd_step(orc, layout, K, gdt):
-    N = 4 * 1501 + 3
+# K not a power of two (3, 5, 12, 17, 33): the tensor layout's step maps
+# lanes to pieces densely, for both gradient types; N = 3 and 5: that
+# mapping with no whole slot, and with one whole slot and a ragged tail.
+@pytest.mark.parametrize("K,gdt,N", [(1, torch.float32, 6007), (3, torch.float32, 6007), (8, torch.bfloat16, 6007),
+                                     (16, torch.float32, 6007), (33, torch.float32, 6007),
+                                     (5, torch.bfloat16, 6007), (12, torch.float32, 6007),
+                                     (17, torch.bfloat16, 6007), (33, torch.bfloat16, 6007),
+                                     (3, torch.float32, 3), (17, torch.bfloat16, 5)])
+def test_sgd_step(orc, layout, K, gdt, N):
     g = tc.Group([N])
     xs, gs = _copies(N, K, torch.float32, K, 0.05), _copies(N, K, gdt, 50 + K, 0.01)
     L = Layout(orc, layout, g, K, xs, gs)
@@ -249,9 +254,11 @@ def test_period_schedule_matches_oracle(orc, layout):
 # slot and a ragged tail; (4, 4099): one copy group of four.  (17, 4099),
 # (33, 100001): K just above a power of two, where the tensor layout's
 # broadcast maps lanes to pieces densely; (3, 2): that mapping with no whole
-# slot, the element tail alone.
+# slot, the element tail alone.  (35, 4005), (33, 2): above K = 32, where
+# 2-byte pieces go two to a lane, with an odd number of pieces (the last
+# lane stores one), and with no whole slot.
 @pytest.mark.parametrize("K,N", [(1, 7), (3, 4097), (8, 100003), (16, 5), (5, 17000003), (1, 4), (1, 1000003),
-                                 (4, 4099), (17, 4099), (33, 100001), (3, 2)])
+                                 (4, 4099), (17, 4099), (33, 100001), (3, 2), (35, 4005), (33, 2)])
 def test_broadcast(orc, layout, dtype, K, N):
     g = tc.Group([N])
     src = torch.randn(N, device=DEV).to(dtype)
