@@ -292,6 +292,40 @@ struct TEasgdArgs {
     int op;
 };
 
+// The trailing partial slot (the last N % 4 elements), element by element.
+template <int P, typename T, bool RED>
+__device__ __forceinline__ void tensor_easgd_tail(const TEasgdArgs<T>& a) {
+    const int K = a.K;
+    const int64_t e = 4 * a.nslot + threadIdx.x;
+    if (e < a.n) {
+        const float cv = a.xc[e];
+        float d[P];
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            if (q < K) {
+                const int64_t idx = (a.nslot * K + q) * 4 + (e & 3);
+                const float xv = a.x[idx];
+                d[q] = xv - cv;
+                a.x[idx] = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, d[q], load_elem(a.g, idx)), xv);
+            } else {
+                d[q] = 0.0f;
+            }
+        }
+        a.xc[e] = __builtin_fmaf(a.a, Tree<P>::sum(d), cv);
+        if constexpr (RED) {
+            // the gradients again, once the center's terms are summed:
+            // holding both sets of P terms would size every lane of the
+            // kernel for them
+            float t[P];
+#pragma unroll
+            for (int q = 0; q < P; ++q) t[q] = q < K ? load_elem(a.g, (a.nslot * K + q) * 4 + (e & 3)) : 0.0f;
+            float r = Tree<P>::sum(t);
+            if (a.op == TC_AVG) r = div_k<P>(r, K);
+            a.out[e] = r;
+        }
+    }
+}
+
 // A wave of the step covers WS = U * 64 / P consecutive slots.  At P >= 16
 // that is at most 8 slots, 128 bytes of the center, which U instructions of
 // 64 / P slots each would read and write in pieces of 16 to 64 bytes; the
@@ -395,36 +429,91 @@ __global__ __launch_bounds__(256) void tensor_easgd_kernel(TEasgdArgs<T> a) {
                 store_slot_pol<TC_TRD_STORE_AUX, I>(a.out, jw + static_cast<I>(lane), rout);
         }
     }
-    if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot
-        const int64_t e = 4 * a.nslot + threadIdx.x;
-        if (e < a.n) {
-            const float cv = a.xc[e];
-            float d[P];
+    if (blockIdx.x == gridDim.x - 1) tensor_easgd_tail<P, T, RED>(a);
+}
+
+// When K is not a power of two, P - K of every P lanes of the slot mapping
+// idle in each load and store.  The staged form moves a workgroup's S slots
+// (S K <= 256 R pieces) between HBM and LDS piece after piece, every lane
+// active but in a last partial round, and runs each
+// slot group's arithmetic on its copies in LDS: the same operations on the
+// same values in the same order as tensor_easgd_kernel, so the results are
+// bit-identical.  The sums over a slot's copies take the split butterfly
+// (each of a group's first four lanes ends with one component).  A slot
+// group's center slot is read by all of its lanes and then overwritten, one
+// component each, by its first four; the group lies in one wave, whose
+// instructions run in order, so every lane reads it first.
+#ifndef TC_TEA_STAGED_MINP
+#define TC_TEA_STAGED_MINP 32
+#endif
+#ifndef TC_TEA_STAGED_R
+#define TC_TEA_STAGED_R 2
+#endif
+template <int P, typename T, int R, typename I, bool RED>
+__global__ __launch_bounds__(256) void tensor_easgd_staged_kernel(TEasgdArgs<T> a, int S) {
+    constexpr int SPB = 256 / P;  // slot groups per pass
+    constexpr int UC = 2 * R;     // passes: S K <= 256 R and K > P / 2 give S < UC SPB
+    __shared__ f4 s_x[256 * R], s_g[256 * R], s_c[UC * SPB], s_r[RED ? UC * SPB : 1];
+    const int K = a.K;
+    const I s0 = static_cast<I>(tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x)) * I(S);
+    const I nslot = static_cast<I>(a.nslot);
+    const int ns = s0 < nslot ? static_cast<int>(nslot - s0 < I(S) ? nslot - s0 : I(S)) : 0;
+    const int np = ns * K;
+    const I p0 = s0 * I(K);
+    f4 vx[R], vg[R];
 #pragma unroll
-            for (int q = 0; q < P; ++q) {
-                if (q < K) {
-                    const int64_t idx = (a.nslot * K + q) * 4 + (e & 3);
-                    const float xv = a.x[idx];
-                    d[q] = xv - cv;
-                    a.x[idx] = __builtin_fmaf(-a.eta, __builtin_fmaf(a.rho, d[q], load_elem(a.g, idx)), xv);
-                } else {
-                    d[q] = 0.0f;
-                }
-            }
-            a.xc[e] = __builtin_fmaf(a.a, Tree<P>::sum(d), cv);
-            if constexpr (RED) {
-                // the gradients again, once the center's terms are summed:
-                // holding both sets of P terms would size every lane of the
-                // kernel for them
-                float t[P];
-#pragma unroll
-                for (int q = 0; q < P; ++q) t[q] = q < K ? load_elem(a.g, (a.nslot * K + q) * 4 + (e & 3)) : 0.0f;
-                float r = Tree<P>::sum(t);
-                if (a.op == TC_AVG) r = div_k<P>(r, K);
-                a.out[e] = r;
-            }
+    for (int u = 0; u < R; ++u) {
+        const int q = threadIdx.x + u * 256;
+        if (q < np) {
+            vx[u] = load_slot(a.x, p0 + I(q));
+            vg[u] = load_slot(a.g, p0 + I(q));
         }
     }
+    if (static_cast<int>(threadIdx.x) < ns) s_c[threadIdx.x] = load_slot(a.xc, s0 + I(threadIdx.x));
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        const int q = threadIdx.x + u * 256;
+        if (q < np) {
+            s_x[q] = vx[u];
+            s_g[q] = vg[u];
+        }
+    }
+    __syncthreads();
+    const int i = threadIdx.x % P;
+    const f4 rho = f4(a.rho), neg_eta = f4(-a.eta);
+#pragma unroll
+    for (int u = 0; u < UC; ++u) {
+        if (u * SPB >= ns) break;  // the same for the whole workgroup
+        const int jl = u * SPB + static_cast<int>(threadIdx.x) / P;
+        const bool slot = jl < ns, live = slot && i < K;
+        const int q = jl * K + i;
+        const f4 x = live ? s_x[q] : f4(0.0f), g = live ? s_g[q] : f4(0.0f);
+        const f4 c = slot ? s_c[jl] : f4(0.0f);
+        const f4 d = live ? x - c : f4(0.0f);
+        const f4 xn = fma4(neg_eta, fma4(rho, d, g), x);
+        const int m = comp_of_lane(i);
+        const float sd = split_group_sum<P>(d, threadIdx.x);
+        const float cm = m == 0 ? c.x : m == 1 ? c.y : m == 2 ? c.z : c.w;
+        if (live) s_x[q] = xn;
+        if (slot && i < 4) reinterpret_cast<float*>(s_c)[jl * 4 + m] = __builtin_fmaf(a.a, sd, cm);
+        if constexpr (RED) {
+            // the gradients of lanes past K are +0
+            float r = split_group_sum<P>(g, threadIdx.x);
+            if (a.op == TC_AVG) r = div_k<P>(r, K);
+            if (slot && i < 4) reinterpret_cast<float*>(s_r)[jl * 4 + m] = r;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        const int q = threadIdx.x + u * 256;
+        if (q < np) store_slot_pol<TC_TEA_X_STORE_AUX, I>(a.x, p0 + I(q), s_x[q]);
+    }
+    if (static_cast<int>(threadIdx.x) < ns) {
+        store_slot_pol<TC_TEA_C_STORE_AUX, I>(a.xc, s0 + I(threadIdx.x), s_c[threadIdx.x]);
+        if constexpr (RED) store_slot_pol<TC_TRD_STORE_AUX, I>(a.out, s0 + I(threadIdx.x), s_r[threadIdx.x]);
+    }
+    if (blockIdx.x == gridDim.x - 1) tensor_easgd_tail<P, T, RED>(a);
 }
 
 // ------------------------------------------ sgd / sync / async / broadcast
@@ -1595,6 +1684,26 @@ hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hip
 
 template <int P, typename T, bool RED>
 hipError_t run_teasgd_as(const TEasgdArgs<T>& a, hipStream_t s) {
+    if constexpr (P >= TC_TEA_STAGED_MINP) {
+        if (a.K != P) {
+            // binary32 gradients: R slot groups' worth of slots, whose pieces
+            // fill K / P of the R rounds; bfloat16: as many as fill them
+            // (P / 2 < K < P).  Measured on MI355X, ResNet-50 group, against
+            // the slot mapping: binary32 step +2-11%, with the reduction
+            // -1 to +14% (K = 17 to 48); filling the rounds lost 3-5 points
+            // of that.  bfloat16 step -1 to +14%, with the reduction +6 to
+            // +30%, where R slot groups had gained up to 14.
+            constexpr int R = TC_TEA_STAGED_R;
+            const int S = sizeof(T) == 4 ? R * (256 / P) : 256 * R / a.K;
+            const int64_t blocks = (a.nslot + S - 1) / S;
+            dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+            if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
+                hipLaunchKernelGGL((tensor_easgd_staged_kernel<P, T, R, uint32_t, RED>), grid, dim3(256), 0, s, a, S);
+            else
+                hipLaunchKernelGGL((tensor_easgd_staged_kernel<P, T, R, int64_t, RED>), grid, dim3(256), 0, s, a, S);
+            return hipGetLastError();
+        }
+    }
     constexpr int U = teasgd_unroll(P);
     constexpr int SPB = 256 / P;
     const int64_t blocks = (a.nslot + SPB * U - 1) / (SPB * U);

@@ -164,10 +164,12 @@ def test_tiny_k2(orc):
     _run(orc, wl.tiny_sizes(), 2, eta=0.1, rho=0.5)
 
 
-@pytest.mark.parametrize("K", [1, 2, 3, 4, 5, 8, 16, 17, 33, 64])
+@pytest.mark.parametrize("K", [1, 2, 3, 4, 5, 8, 12, 16, 17, 20, 33, 64])
 def test_k_and_ragged_tail(orc, K):
     """Several tiles and chunks, a group length that is not a multiple of 4,
-    zero-size tensors, and tensors that end inside a slot."""
+    zero-size tensors, and tensors that end inside a slot.  At K = 12, 17,
+    20 and 33 the four calls' step is the LDS-staged kernel, so this also
+    holds it bit for bit to the pipelined kernel's own slot-group step."""
     sizes = [3000, 0, 5, 4096, 1, 0, 7, 9001, 2, 20003]
     _run(orc, sizes, K, seed=K)
 
