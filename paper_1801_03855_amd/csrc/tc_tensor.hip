@@ -228,6 +228,21 @@ __device__ __forceinline__ f4 load_pair_sum(const uint16_t* p, I s) {
     return lo + hi;
 }
 
+// The trailing partial slot (the last N % 4 elements), element by element.
+template <int P, typename T>
+__device__ __forceinline__ void tensor_reduce_tail(const TReduceArgs<T>& a) {
+    const int K = a.K;
+    const int64_t e = 4 * a.nslot + threadIdx.x;
+    if (e < a.n) {
+        float t[P];
+#pragma unroll
+        for (int q = 0; q < P; ++q) t[q] = q < K ? load_elem(a.in, (a.nslot * K + q) * 4 + (e & 3)) : 0.0f;
+        float s = Tree<P>::sum(t);
+        if (a.op == TC_AVG) s = div_k<P>(s, K);
+        a.out[e] = s;
+    }
+}
+
 // P: K rounded up to a power of two.  One lane per copy (L = P lanes per
 // slot), or, for bfloat16 with K even (PAIR), one lane per two copies
 // (L = P / 2): each lane loads 16 bytes and adds its pair first, which is
@@ -264,18 +279,115 @@ __global__ __launch_bounds__(256) void tensor_reduce_kernel(TReduceArgs<T> a) {
             if (j < nslot && i == 0) store_slot_pol<TC_TRD_STORE_AUX, I>(a.out, j, s);
         }
     }
-    if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot
-        const int64_t e = 4 * a.nslot + threadIdx.x;
-        if (e < a.n) {
-            float t[P];
+    if (blockIdx.x == gridDim.x - 1) tensor_reduce_tail<P, T>(a);
+}
+
+// The reduction staged through LDS, as the fused step is: a workgroup's S
+// slots (S K <= 256 R pieces) are read piece after piece, every lane active,
+// and each slot group's split butterfly runs on its copies in LDS, with the
+// slot kernel's operations and order.  It serves bfloat16 copies at odd K
+// (P >= 8), where the slot kernel reads one 8-byte copy per lane: the pieces
+// come in two to a lane with 16-byte loads (S even keeps the workgroup's
+// first piece 16-byte aligned), and each lane adds copies 2i and 2i + 1, the
+// pairwise tree's first level, before a butterfly over P / 2 lanes.
+// Measured on MI355X, ResNet-50 group, against the slot kernel: K = 5 to 13
+// 3.3-4.5 -> 6.0-6.4 TB/s, K = 17 to 63 1.9-2.7 -> 5.1-6.4; 8 rounds of 256
+// pieces per workgroup against 2, 4, 6, 12 and 16.  For binary32 copies
+// (P >= 32) it measured 5-18% slower and is off.
+#ifndef TC_TRD_STAGED_R
+#define TC_TRD_STAGED_R 8
+#endif
+#ifndef TC_TRD_STAGED_F32
+#define TC_TRD_STAGED_F32 0
+#endif
+#ifndef TC_TRD_STAGED_BF16
+#define TC_TRD_STAGED_BF16 1
+#endif
+#ifndef TC_TRD_STAGED_WIDE
+#define TC_TRD_STAGED_WIDE 1
+#endif
+#ifndef TC_TRD_STAGED_BF16_MINP
+#define TC_TRD_STAGED_BF16_MINP 8
+#endif
+template <int P, typename T, int R, typename I, bool PAIR>
+__global__ __launch_bounds__(256) void tensor_reduce_staged_kernel(TReduceArgs<T> a, int S) {
+    constexpr int L = PAIR ? P / 2 : P;  // lanes per slot group
+    constexpr int SPB = 256 / L;         // slot groups per pass
+    constexpr int UC = 2 * R * L / P;    // passes: S K <= 256 R and K > P / 2 give S < UC SPB
+    using V = typename std::conditional<sizeof(T) == 4, u4, u2>::type;  // a stored piece
+    __shared__ V s_v[256 * R];
+    const int K = a.K;
+    const I s0 = static_cast<I>(tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x)) * I(S);
+    const I nslot = static_cast<I>(a.nslot);
+    const int ns = s0 < nslot ? static_cast<int>(nslot - s0 < I(S) ? nslot - s0 : I(S)) : 0;
+    const int np = ns * K;
+    const I p0 = s0 * I(K);
+    if constexpr (sizeof(T) == 2 && TC_TRD_STAGED_WIDE) {
+        // 8-byte pieces two to a lane, one 16-byte load (S is even, so the
+        // workgroup's first piece is 16-byte aligned)
+        constexpr int R2 = (R + 1) / 2;
+        u4 w[R2];
+        const char* base = reinterpret_cast<const char*>(a.in) + p0 * I(8);
 #pragma unroll
-            for (int q = 0; q < P; ++q)
-                t[q] = q < K ? load_elem(a.in, (a.nslot * K + q) * 4 + (e & 3)) : 0.0f;
-            float s = Tree<P>::sum(t);
-            if (a.op == TC_AVG) s = div_k<P>(s, K);
-            a.out[e] = s;
+        for (int u = 0; u < R2; ++u) {
+            const int q = 2 * (threadIdx.x + u * 256);
+            if (q + 1 < np) w[u] = __builtin_nontemporal_load(reinterpret_cast<const u4*>(base + q * 8));
+            else if (q < np) {
+                const u2 h = __builtin_nontemporal_load(reinterpret_cast<const u2*>(base + q * 8));
+                w[u] = u4{h.x, h.y, 0u, 0u};
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < R2; ++u) {
+            const int q = 2 * (threadIdx.x + u * 256);
+            if (q < np) s_v[q] = V{w[u].x, w[u].y};
+            if (q + 1 < np) s_v[q + 1] = V{w[u].z, w[u].w};
+        }
+    } else {
+        V v[R];
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            const int q = threadIdx.x + u * 256;
+            if (q < np)
+                v[u] = __builtin_nontemporal_load(
+                    reinterpret_cast<const V*>(reinterpret_cast<const char*>(a.in) + (p0 + I(q)) * I(sizeof(V))));
+        }
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            const int q = threadIdx.x + u * 256;
+            if (q < np) s_v[q] = v[u];
         }
     }
+    __syncthreads();
+    auto piece = [&](int q) -> f4 {
+        const V w = s_v[q];
+        if constexpr (sizeof(T) == 4)
+            return f4{__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w)};
+        else
+            return f4{__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u), __uint_as_float(w.y << 16),
+                      __uint_as_float(w.y & 0xffff0000u)};
+    };
+    const int i = threadIdx.x % L;
+#pragma unroll
+    for (int u = 0; u < UC; ++u) {
+        if (u * SPB >= ns) break;  // the same for the whole workgroup
+        const int jl = u * SPB + static_cast<int>(threadIdx.x) / L;
+        const bool slot = jl < ns;
+        f4 x = f4(0.0f);
+        if constexpr (PAIR) {
+            // copies 2i and 2i + 1 added in the lane: the pairwise tree's
+            // first level (a missing last copy is the tree's +0 padding)
+            const f4 lo = slot && 2 * i < K ? piece(jl * K + 2 * i) : f4(0.0f);
+            const f4 hi = slot && 2 * i + 1 < K ? piece(jl * K + 2 * i + 1) : f4(0.0f);
+            x = lo + hi;
+        } else if (slot && i < K) {
+            x = piece(jl * K + i);
+        }
+        float r = split_group_sum<L>(x, threadIdx.x);
+        if (a.op == TC_AVG) r = div_k<P>(r, K);
+        if (slot && i < 4) store_elem_pol<TC_TRD_STORE_AUX, I>(a.out, s0 + I(jl), comp_of_lane(i), r);
+    }
+    if (blockIdx.x == gridDim.x - 1) tensor_reduce_tail<P, T>(a);
 }
 
 // --------------------------------------------------------------- easgd
@@ -533,6 +645,40 @@ struct TStepArgs {
 
 enum class TOp { Sgd, Sync, Async };
 
+// The trailing partial slot (the last N % 4 elements), element by element.
+template <TOp OP, int P, typename T>
+__device__ __forceinline__ void tensor_step_tail(const TStepArgs<T>& a) {
+    const int K = a.K;
+    const int64_t e = 4 * a.nslot + threadIdx.x;
+    if (e < a.n) {
+        auto idx = [&](int q) { return (a.nslot * K + q) * 4 + (e & 3); };
+        if constexpr (OP == TOp::Sgd) {
+            for (int q = 0; q < K; ++q)
+                a.x[idx(q)] = __builtin_fmaf(-a.s0, load_elem(static_cast<const T*>(a.g), idx(q)), a.x[idx(q)]);
+        } else if constexpr (OP == TOp::Sync) {
+            float t[P];
+#pragma unroll
+            for (int q = 0; q < P; ++q) t[q] = q < K ? load_elem(static_cast<const T*>(a.g), idx(q)) : 0.0f;
+            const float S = Tree<P>::sum(t);
+            for (int q = 0; q < K; ++q) {
+                a.x[idx(q)] = __builtin_fmaf(-a.s0, S, a.x[idx(q)]);
+                if constexpr (sizeof(T) == 4)
+                    if (a.flag) reinterpret_cast<float*>(a.g)[idx(q)] = S;
+            }
+        } else {
+            float c = a.xc[e];
+            for (int r = 0; r < a.R; ++r) {
+                const int64_t k = idx(a.order[r]);
+                const float d = a.x[k] - c;
+                c = __builtin_fmaf(a.s0, d, c);
+                a.x[k] = __builtin_fmaf(-a.s0, d, a.x[k]);
+            }
+            a.xc[e] = c;
+        }
+    }
+}
+
+
 
 
 template <TOp OP, int P, typename T, typename I>
@@ -584,35 +730,7 @@ __global__ __launch_bounds__(256) void tensor_step_kernel(TStepArgs<T> a) {
         if (live && mine) store_slot(a.x, piece, fma4(f4(-a.s0), d_mine, x));
         if (slot && i == 0) store_slot(a.xc, j, c);
     }
-    if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot, element by element
-        const int64_t e = 4 * a.nslot + threadIdx.x;
-        if (e < a.n) {
-            auto idx = [&](int q) { return (a.nslot * K + q) * 4 + (e & 3); };
-            if constexpr (OP == TOp::Sgd) {
-                for (int q = 0; q < K; ++q)
-                    a.x[idx(q)] = __builtin_fmaf(-a.s0, load_elem(static_cast<const T*>(a.g), idx(q)), a.x[idx(q)]);
-            } else if constexpr (OP == TOp::Sync) {
-                float t[P];
-#pragma unroll
-                for (int q = 0; q < P; ++q) t[q] = q < K ? load_elem(static_cast<const T*>(a.g), idx(q)) : 0.0f;
-                const float S = Tree<P>::sum(t);
-                for (int q = 0; q < K; ++q) {
-                    a.x[idx(q)] = __builtin_fmaf(-a.s0, S, a.x[idx(q)]);
-                    if constexpr (sizeof(T) == 4)
-                        if (a.flag) reinterpret_cast<float*>(a.g)[idx(q)] = S;
-                }
-            } else {
-                float c = a.xc[e];
-                for (int r = 0; r < a.R; ++r) {
-                    const int64_t k = idx(a.order[r]);
-                    const float d = a.x[k] - c;
-                    c = __builtin_fmaf(a.s0, d, c);
-                    a.x[k] = __builtin_fmaf(-a.s0, d, a.x[k]);
-                }
-                a.xc[e] = c;
-            }
-        }
-    }
+    if (blockIdx.x == gridDim.x - 1) tensor_step_tail<OP, P, T>(a);
 }
 
 // The asynchronous exchange at P >= 4.  The center's recurrence over the
@@ -1677,6 +1795,23 @@ hipError_t run_treduce_as(int K, const void* in, float* out, int op, int64_t n, 
 
 template <int P, typename T>
 hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hipStream_t s) {
+    if constexpr (P >= (sizeof(T) == 4 ? 32 : TC_TRD_STAGED_BF16_MINP)) {
+        const bool staged = sizeof(T) == 4 ? TC_TRD_STAGED_F32 && K != P : TC_TRD_STAGED_BF16 && K % 2 == 1;
+        if (staged) {
+            // as many slots as fill R rounds of the 256 lanes (P / 2 < K < P)
+            constexpr int R = TC_TRD_STAGED_R;
+            const int S = (256 * R / K) & ~(sizeof(T) == 2 && TC_TRD_STAGED_WIDE ? 1 : 0);
+            TReduceArgs<T> a{static_cast<const T*>(in), out, n / 4, n, K, op};
+            const int64_t blocks = (a.nslot + S - 1) / S;
+            dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+            constexpr bool PAIR = sizeof(T) == 2;  // bfloat16: two copies a lane
+            if ((a.nslot + 1) * K * 16 < (int64_t(1) << 32))
+                hipLaunchKernelGGL((tensor_reduce_staged_kernel<P, T, R, uint32_t, PAIR>), grid, dim3(256), 0, s, a, S);
+            else
+                hipLaunchKernelGGL((tensor_reduce_staged_kernel<P, T, R, int64_t, PAIR>), grid, dim3(256), 0, s, a, S);
+            return hipGetLastError();
+        }
+    }
     if constexpr (sizeof(T) == 2 && P >= 2)
         if (TC_TREDUCE_PAIR && K % 2 == 0) return run_treduce_as<P, T, true>(K, in, out, op, n, s);
     return run_treduce_as<P, T, false>(K, in, out, op, n, s);
@@ -1938,21 +2073,94 @@ __global__ __launch_bounds__(256) void tensor_sgd_dense_kernel(TStepArgs<T> a) {
         const f4 x = load_slot(a.x, p), g = load_slot(static_cast<const T*>(a.g), p);
         store_slot(a.x, p, fma4(f4(-a.s0), g, x));
     }
-    if (blockIdx.x == gridDim.x - 1) {  // trailing partial slot, element by element
-        const int64_t e = 4 * a.nslot + threadIdx.x;
-        if (e < a.n)
-            for (int q = 0; q < a.K; ++q) {
-                const int64_t k = (a.nslot * a.K + q) * 4 + (e & 3);
-                a.x[k] = __builtin_fmaf(-a.s0, load_elem(static_cast<const T*>(a.g), k), a.x[k]);
-            }
+    if (blockIdx.x == gridDim.x - 1) tensor_step_tail<TOp::Sgd, 1, T>(a);  // P is not used by plain SGD
+}
+
+// Synchronous SGD staged through LDS (P >= 32, K not a power of two), as
+// the fused step is: the slot kernel's sum (the full butterfly) and update
+// on the copies in LDS, the workers and the broadcast sums written back
+// piece after piece.
+template <int P, typename T, int R, typename I>
+__global__ __launch_bounds__(256) void tensor_sync_staged_kernel(TStepArgs<T> a, int S) {
+    constexpr int SPB = 256 / P;  // slot groups per pass
+    constexpr int UC = 2 * R;     // passes: S K <= 256 R and K > P / 2 give S < UC SPB
+    __shared__ f4 s_x[256 * R], s_g[256 * R];
+    const int K = a.K;
+    const I s0 = static_cast<I>(tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x)) * I(S);
+    const I nslot = static_cast<I>(a.nslot);
+    const int ns = s0 < nslot ? static_cast<int>(nslot - s0 < I(S) ? nslot - s0 : I(S)) : 0;
+    const int np = ns * K;
+    const I p0 = s0 * I(K);
+    const bool bcast = sizeof(T) == 4 && a.flag;
+    f4 vx[R], vg[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        const int q = threadIdx.x + u * 256;
+        if (q < np) {
+            vx[u] = load_slot(a.x, p0 + I(q));
+            vg[u] = load_slot(static_cast<const T*>(a.g), p0 + I(q));
+        }
     }
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        const int q = threadIdx.x + u * 256;
+        if (q < np) {
+            s_x[q] = vx[u];
+            s_g[q] = vg[u];
+        }
+    }
+    __syncthreads();
+    const int i = threadIdx.x % P;
+#pragma unroll
+    for (int u = 0; u < UC; ++u) {
+        if (u * SPB >= ns) break;  // the same for the whole workgroup
+        const int jl = u * SPB + static_cast<int>(threadIdx.x) / P;
+        const bool live = jl < ns && i < K;
+        const int q = jl * K + i;
+        const f4 g = live ? s_g[q] : f4(0.0f), x = live ? s_x[q] : f4(0.0f);
+        const f4 sum = group_sum4<P>(g);
+        if (live) {
+            s_x[q] = fma4(f4(-a.s0), sum, x);
+            if (bcast) s_g[q] = sum;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        const int q = threadIdx.x + u * 256;
+        if (q < np) {
+            store_slot(a.x, p0 + I(q), s_x[q]);
+            if constexpr (sizeof(T) == 4)
+                if (bcast) store_slot(reinterpret_cast<float*>(a.g), p0 + I(q), s_g[q]);
+        }
+    }
+    if (blockIdx.x == gridDim.x - 1) tensor_step_tail<TOp::Sync, P, T>(a);
 }
 
 #ifndef TC_TSGD_DENSE
 #define TC_TSGD_DENSE 1
 #endif
+#ifndef TC_TSYNC_STAGED
+#define TC_TSYNC_STAGED 1
+#endif
 template <TOp OP, int P, typename T>
 hipError_t run_tstep(const TStepArgs<T>& a, hipStream_t s) {
+    if constexpr (OP == TOp::Sync && P >= 32) {
+        // bfloat16 gradients: every K between powers of two; binary32: only
+        // where more than 7/16 of the slot mapping's lanes would idle
+        if (TC_TSYNC_STAGED && a.K != P && (sizeof(T) == 2 || (P - a.K) * 16 > 7 * P)) {
+            // slots per workgroup as for the staged fused step (P / 2 < K < P)
+            constexpr int R = TC_TEA_STAGED_R;
+            const int S = sizeof(T) == 4 ? R * (256 / P) : 256 * R / a.K;
+            const int64_t blocks = (a.nslot + S - 1) / S;
+            dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+            if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
+                hipLaunchKernelGGL((tensor_sync_staged_kernel<P, T, R, uint32_t>), grid, dim3(256), 0, s, a, S);
+            else
+                hipLaunchKernelGGL((tensor_sync_staged_kernel<P, T, R, int64_t>), grid, dim3(256), 0, s, a, S);
+            return hipGetLastError();
+        }
+    }
     if constexpr (OP == TOp::Sgd) {
         if (TC_TSGD_DENSE && a.K != P) {
             const int64_t blocks = (a.nslot * a.K + 255) / 256;

@@ -165,8 +165,11 @@ def test_elastic_async_exact_regime(orc, layout, K):
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
+# K = 17, 20, 33, 48: the tensor layout's step staged through LDS
 @pytest.mark.parametrize("K,gdt,bcast", [(1, torch.float32, True), (4, torch.float32, True), (8, torch.float32, False),
-                                         (16, torch.bfloat16, False), (20, torch.float32, True)])
+                                         (16, torch.bfloat16, False), (20, torch.float32, True),
+                                         (17, torch.float32, False), (33, torch.bfloat16, False),
+                                         (48, torch.float32, True)])
 def test_sync_sgd(orc, layout, K, gdt, bcast):
     N = 4 * 2001 + 1
     g = tc.Group([N])
@@ -194,6 +197,27 @@ def test_sync_sgd(orc, layout, K, gdt, bcast):
     else:
         for a, b in zip(L.g_host(), h_g):
             assert_bits_equal(a, b, "gradients untouched")
+
+
+@pytest.mark.parametrize("K", [8, 17, 33, 48])
+def test_sync_sgd_tensor_sums_equal_the_reduction(orc, K):
+    """The broadcast sums of the tensor-layout synchronous step (a full
+    butterfly per slot group) equal tc_reduce_tensor's SUM (a split
+    butterfly) bit for bit: both add a slot's copies in the pairwise tree
+    over P terms, padded with +0.  From K = 17 on, both kernels are staged
+    through LDS."""
+    N = 4 * 3001 + 2
+    g = tc.Group([N])
+    gs = _copies(N, K, torch.float32, 300 + K, 0.01)
+    xs = [torch.zeros(N, device=DEV) for _ in range(K)]
+    L = Layout(orc, "tensor", g, K, xs, gs)
+    ref = torch.empty(N, device=DEV)
+    tc.reduce_tensor(g, K, L.G, ref, "sum")
+    tc.sync_sgd_step_tensor(g, K, L.X, L.G, 0.5, 1.0, True)
+    torch.cuda.synchronize()
+    r = host_f32(ref)
+    for i, gi in enumerate(L.g_host()):
+        assert_bits_equal(gi, r, f"K={K} broadcast g[{i}] vs tc_reduce_tensor")
 
 
 def test_sync_sgd_bf16_broadcast_unsupported():
