@@ -285,29 +285,25 @@ __global__ __launch_bounds__(256) void tensor_reduce_kernel(TReduceArgs<T> a) {
 // The reduction staged through LDS, as the fused step is: a workgroup's S
 // slots (S K <= 256 R pieces) are read piece after piece, every lane active,
 // and each slot group's split butterfly runs on its copies in LDS, with the
-// slot kernel's operations and order.  It serves bfloat16 copies at odd K
-// (P >= 8), where the slot kernel reads one 8-byte copy per lane: the pieces
-// come in two to a lane with 16-byte loads (S even keeps the workgroup's
-// first piece 16-byte aligned), and each lane adds copies 2i and 2i + 1, the
-// pairwise tree's first level, before a butterfly over P / 2 lanes.
-// Measured on MI355X, ResNet-50 group, against the slot kernel: K = 5 to 13
-// 3.3-4.5 -> 6.0-6.4 TB/s, K = 17 to 63 1.9-2.7 -> 5.1-6.4; 8 rounds of 256
-// pieces per workgroup against 2, 4, 6, 12 and 16.  For binary32 copies
-// (P >= 32) it measured 5-18% slower and is off.
+// slot kernel's operations and order.  It serves bfloat16 copies at K not a
+// power of two (P >= 8), where the slot kernel reads one 8-byte copy per
+// lane (odd K) or idles lanes: the pieces come in two to a lane with 16-byte
+// loads (S even keeps the workgroup's first piece 16-byte aligned), and each
+// lane adds copies 2i and 2i + 1, the pairwise tree's first level, before a
+// butterfly over P / 2 lanes.  Measured on MI355X, ResNet-50 group, against
+// the slot kernels: odd K = 5 to 13 3.3-4.5 -> 6.0-6.4 TB/s, K = 17 to 63
+// 1.9-2.7 -> 5.1-6.4; even K = 6 to 48 +3-32%; 8 rounds of 256 pieces per
+// workgroup against 2, 4, 6, 12 and 16.  For binary32 copies (P >= 32) the
+// staged form measured 5-18% slower with one copy per lane, -4 to +2.5%
+// with pairs, and is not used.
 #ifndef TC_TRD_STAGED_R
 #define TC_TRD_STAGED_R 8
 #endif
-#ifndef TC_TRD_STAGED_F32
-#define TC_TRD_STAGED_F32 0
+#ifndef TC_TRD_STAGED
+#define TC_TRD_STAGED 1
 #endif
-#ifndef TC_TRD_STAGED_BF16
-#define TC_TRD_STAGED_BF16 1
-#endif
-#ifndef TC_TRD_STAGED_WIDE
-#define TC_TRD_STAGED_WIDE 1
-#endif
-#ifndef TC_TRD_STAGED_BF16_MINP
-#define TC_TRD_STAGED_BF16_MINP 8
+#ifndef TC_TRD_STAGED_MINP
+#define TC_TRD_STAGED_MINP 8
 #endif
 template <int P, typename T, int R, typename I, bool PAIR>
 __global__ __launch_bounds__(256) void tensor_reduce_staged_kernel(TReduceArgs<T> a, int S) {
@@ -322,7 +318,7 @@ __global__ __launch_bounds__(256) void tensor_reduce_staged_kernel(TReduceArgs<T
     const int ns = s0 < nslot ? static_cast<int>(nslot - s0 < I(S) ? nslot - s0 : I(S)) : 0;
     const int np = ns * K;
     const I p0 = s0 * I(K);
-    if constexpr (sizeof(T) == 2 && TC_TRD_STAGED_WIDE) {
+    if constexpr (sizeof(T) == 2) {
         // 8-byte pieces two to a lane, one 16-byte load (S is even, so the
         // workgroup's first piece is 16-byte aligned)
         constexpr int R2 = (R + 1) / 2;
@@ -1795,16 +1791,16 @@ hipError_t run_treduce_as(int K, const void* in, float* out, int op, int64_t n, 
 
 template <int P, typename T>
 hipError_t run_treduce(int K, const void* in, float* out, int op, int64_t n, hipStream_t s) {
-    if constexpr (P >= (sizeof(T) == 4 ? 32 : TC_TRD_STAGED_BF16_MINP)) {
-        const bool staged = sizeof(T) == 4 ? TC_TRD_STAGED_F32 && K != P : TC_TRD_STAGED_BF16 && K % 2 == 1;
-        if (staged) {
-            // as many slots as fill R rounds of the 256 lanes (P / 2 < K < P)
+    if constexpr (sizeof(T) == 2 && P >= TC_TRD_STAGED_MINP) {
+        if (TC_TRD_STAGED && K != P) {
+            // as many slots as fill R rounds of the 256 lanes (P / 2 < K < P),
+            // rounded down to even
             constexpr int R = TC_TRD_STAGED_R;
-            const int S = (256 * R / K) & ~(sizeof(T) == 2 && TC_TRD_STAGED_WIDE ? 1 : 0);
+            const int S = (256 * R / K) & ~1;
             TReduceArgs<T> a{static_cast<const T*>(in), out, n / 4, n, K, op};
             const int64_t blocks = (a.nslot + S - 1) / S;
             dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
-            constexpr bool PAIR = sizeof(T) == 2;  // bfloat16: two copies a lane
+            constexpr bool PAIR = true;  // two copies a lane
             if ((a.nslot + 1) * K * 16 < (int64_t(1) << 32))
                 hipLaunchKernelGGL((tensor_reduce_staged_kernel<P, T, R, uint32_t, PAIR>), grid, dim3(256), 0, s, a, S);
             else

@@ -188,13 +188,15 @@ def test_reduce_tensor(orc, K, dtype):
         assert_close(host_f32(out), orc.reduce(copies, code), reduce_mag(copies, op == "avg"), f"K={K} {op}")
 
 
-@pytest.mark.parametrize("K", [2, 3, 6, 16, 33, 64])
+@pytest.mark.parametrize("K", [2, 3, 6, 10, 16, 18, 24, 33, 64])
 def test_reduce_tensor_bf16_pairs(orc, K):
     """bfloat16 copies with K even are read two per lane, which adds each
-    pair before the butterfly (the pairwise tree's first level).  Both
-    layouts add in that tree, so the tensor layout's SUM and AVG equal the
-    separate-buffer reduction bit for bit on general inputs; integers that
-    bfloat16 holds exactly (|v| <= 256) give the oracle's sums exactly."""
+    pair before the butterfly (the pairwise tree's first level); at K not a
+    power of two (6, 10, 18, 24, 33) the copies are staged through LDS and
+    paired there, odd K included.  Both layouts add in that tree, so the
+    tensor layout's SUM and AVG equal the separate-buffer reduction bit for
+    bit on general inputs; integers that bfloat16 holds exactly
+    (|v| <= 256) give the oracle's sums exactly."""
     N = 4 * 2053 + 1
     g = tc.Group([N])
     for name, copies in (("general", _make_copies(N, K, torch.bfloat16, seed=40 + K)),
