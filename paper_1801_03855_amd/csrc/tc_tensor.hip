@@ -808,6 +808,87 @@ __global__ __launch_bounds__(256) void tensor_async_kernel(TStepArgs<float> a) {
     }
 }
 
+// The asynchronous exchange staged through LDS (K >= TC_TASYNC_STAGED_K).
+// In tensor_async_kernel only lanes 0-3 of each slot group run the
+// recurrence, 8 of a wave's 64 lanes at P = 64.  Here a workgroup reads its
+// S slots into LDS piece after piece, every lane active, one row of KP = K
+// | 1 pieces per slot (an odd row length puts the rows' component i in
+// distinct banks), and every lane runs V of the workgroup's 4 S scalar
+// recurrences (one per slot and component), updating each exchanged worker
+// in place: d = x_w - c, c = fma(alpha, d, c), x_w = fma(-alpha, d, x_w),
+// the slot kernel's operations in its order.  The exchanged workers' pieces
+// are then written back piece after piece.  Measured on MI355X, ResNet-50
+// group, R = K, against the slot kernel: K = 33 2.96 -> 3.80 TB/s, K = 40
+// +17%, K = 48 +4%, K = 64 +5%; at K = 17 to 32, where the slot kernel runs
+// at 4.7-5.6, it stays at 3.7-3.9 (the phases of a workgroup run one after
+// another, and its 64 KiB of LDS leave room for two per CU), so it starts at
+// K = 33.  One or four recurrences per lane measured below two.
+#ifndef TC_TASYNC_STAGED_K
+#define TC_TASYNC_STAGED_K 33
+#endif
+#ifndef TC_TASYNC_STAGED_V
+#define TC_TASYNC_STAGED_V 2
+#endif
+constexpr int kAsyncStagedPieces = 4096;  // LDS pieces per workgroup (64 KiB)
+template <int V, typename I>
+__global__ __launch_bounds__(256) void tensor_async_staged_kernel(TStepArgs<float> a, int S) {
+    __shared__ f4 s_x[kAsyncStagedPieces];  // S rows of KP pieces
+    const int K = a.K, KP = K | 1;
+    const I s0 = static_cast<I>(tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x)) * I(S);
+    const I nslot = static_cast<I>(a.nslot);
+    const int ns = s0 < nslot ? static_cast<int>(nslot - s0 < I(S) ? nslot - s0 : I(S)) : 0;
+    const int np = ns * K;
+    const I p0 = s0 * I(K);
+    // pieces in, four loads in flight per lane
+    for (int q0 = 0; q0 < np; q0 += 4 * 256) {
+        f4 v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int q = q0 + t * 256 + static_cast<int>(threadIdx.x);
+            if (q < np) v[t] = load_slot(a.x, p0 + I(q));
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int q = q0 + t * 256 + static_cast<int>(threadIdx.x);
+            if (q < np) s_x[(q / K) * KP + q % K] = v[t];
+        }
+    }
+    float c[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        const int ch = static_cast<int>(threadIdx.x) + v * 256;  // slot ch / 4, component ch % 4
+        c[v] = ch < 4 * ns ? __builtin_nontemporal_load(a.xc + ((s0 + I(ch / 4)) * I(4) + I(ch % 4))) : 0.0f;
+    }
+    __syncthreads();
+    float* sx = reinterpret_cast<float*>(s_x);
+#pragma unroll 2
+    for (int r = 0; r < a.R; ++r) {
+        const int w = a.order[r];
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            const int ch = static_cast<int>(threadIdx.x) + v * 256;
+            if (ch < 4 * ns) {
+                float* px = sx + ((ch / 4) * KP + w) * 4 + ch % 4;
+                const float xw = *px;
+                const float d = xw - c[v];
+                c[v] = __builtin_fmaf(a.s0, d, c[v]);
+                *px = __builtin_fmaf(-a.s0, d, xw);
+            }
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        const int ch = static_cast<int>(threadIdx.x) + v * 256;
+        if (ch < 4 * ns) __builtin_nontemporal_store(c[v], a.xc + ((s0 + I(ch / 4)) * I(4) + I(ch % 4)));
+    }
+    __syncthreads();
+    for (int q = static_cast<int>(threadIdx.x); q < np; q += 256) {
+        const int w = q % K;
+        if ((a.exchanged >> w) & 1) store_slot(a.x, p0 + I(q), s_x[(q / K) * KP + w]);
+    }
+    if (blockIdx.x == gridDim.x - 1) tensor_step_tail<TOp::Async, 64, float>(a);  // P is not used by the exchange
+}
+
 // Broadcast of one flat buffer into every copy of a tensor-layout buffer.
 // A lane takes U slots of its copy (a wave U*64/P adjacent slots) and issues
 // all U source loads before its stores.  Measured on MI355X with sources
@@ -2165,6 +2246,20 @@ hipError_t run_tstep(const TStepArgs<T>& a, hipStream_t s) {
                 hipLaunchKernelGGL((tensor_sgd_dense_kernel<T, uint32_t>), grid, dim3(256), 0, s, a);
             else
                 hipLaunchKernelGGL((tensor_sgd_dense_kernel<T, int64_t>), grid, dim3(256), 0, s, a);
+            return hipGetLastError();
+        }
+    }
+    if constexpr (OP == TOp::Async && sizeof(T) == 4) {
+        if (a.K >= TC_TASYNC_STAGED_K) {
+            constexpr int V = TC_TASYNC_STAGED_V;
+            const int KP = a.K | 1;
+            const int S = 64 * V < kAsyncStagedPieces / KP ? 64 * V : kAsyncStagedPieces / KP;
+            const int64_t blocks = (a.nslot + S - 1) / S;
+            dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+            if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
+                hipLaunchKernelGGL((tensor_async_staged_kernel<V, uint32_t>), grid, dim3(256), 0, s, a, S);
+            else
+                hipLaunchKernelGGL((tensor_async_staged_kernel<V, int64_t>), grid, dim3(256), 0, s, a, S);
             return hipGetLastError();
         }
     }

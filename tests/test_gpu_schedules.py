@@ -91,7 +91,8 @@ def test_sgd_step(orc, layout, K, gdt, N):
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
-@pytest.mark.parametrize("K", [1, 2, 5, 8, 16, 40])
+# K = 33 and 40: the exchange staged through LDS
+@pytest.mark.parametrize("K", [1, 2, 5, 8, 16, 33, 40])
 def test_elastic_async(orc, layout, K):
     N = 4 * 1025 + 2
     g = tc.Group([N])
