@@ -817,22 +817,23 @@ __global__ __launch_bounds__(256) void tensor_async_kernel(TStepArgs<float> a) {
 // recurrences (one per slot and component), updating each exchanged worker
 // in place: d = x_w - c, c = fma(alpha, d, c), x_w = fma(-alpha, d, x_w),
 // the slot kernel's operations in its order.  The exchanged workers' pieces
-// are then written back piece after piece.  Measured on MI355X, ResNet-50
-// group, R = K, against the slot kernel: K = 33 2.96 -> 3.80 TB/s, K = 40
-// +17%, K = 48 +4%, K = 64 +5%; at K = 17 to 32, where the slot kernel runs
-// at 4.7-5.6, it stays at 3.7-3.9 (the phases of a workgroup run one after
-// another, and its 64 KiB of LDS leave room for two per CU), so it starts at
-// K = 33.  One or four recurrences per lane measured below two.
-#ifndef TC_TASYNC_STAGED_K
-#define TC_TASYNC_STAGED_K 33
+// are then written back piece after piece.  The LDS is sized at launch to
+// the S rows, so that smaller K fit more workgroups per CU.  Measured on
+// MI355X, ResNet-50 group, R = K, against the slot kernel: K = 17 +19%,
+// K = 33 2.96 -> 5.08 TB/s, K = 40 and 48 +26-27%, K = 64 level; K = 24 -3%
+// and K = 32 -13%.  So it takes K between powers of two from 33, and from 17
+// while more than a quarter of the slot mapping's lanes would idle.  Two or
+// four recurrences per lane (twice or four times the rows) measured slower.
+#ifndef TC_TASYNC_STAGED
+#define TC_TASYNC_STAGED 1
 #endif
 #ifndef TC_TASYNC_STAGED_V
-#define TC_TASYNC_STAGED_V 2
+#define TC_TASYNC_STAGED_V 1
 #endif
 constexpr int kAsyncStagedPieces = 4096;  // LDS pieces per workgroup (64 KiB)
 template <int V, typename I>
 __global__ __launch_bounds__(256) void tensor_async_staged_kernel(TStepArgs<float> a, int S) {
-    __shared__ f4 s_x[kAsyncStagedPieces];  // S rows of KP pieces
+    extern __shared__ f4 s_x[];  // S rows of KP pieces (sized at launch)
     const int K = a.K, KP = K | 1;
     const I s0 = static_cast<I>(tile_of<TC_XCD_RUN_STEP>(blockIdx.x, gridDim.x)) * I(S);
     const I nslot = static_cast<I>(a.nslot);
@@ -2249,17 +2250,18 @@ hipError_t run_tstep(const TStepArgs<T>& a, hipStream_t s) {
             return hipGetLastError();
         }
     }
-    if constexpr (OP == TOp::Async && sizeof(T) == 4) {
-        if (a.K >= TC_TASYNC_STAGED_K) {
+    if constexpr (OP == TOp::Async && sizeof(T) == 4 && P >= 32) {
+        if (TC_TASYNC_STAGED && a.K != P && (P >= 64 || (P - a.K) * 4 > P)) {
             constexpr int V = TC_TASYNC_STAGED_V;
             const int KP = a.K | 1;
             const int S = 64 * V < kAsyncStagedPieces / KP ? 64 * V : kAsyncStagedPieces / KP;
             const int64_t blocks = (a.nslot + S - 1) / S;
             dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
+            const size_t lds = static_cast<size_t>(S) * KP * sizeof(f4);
             if ((a.nslot + 1) * a.K * 16 < (int64_t(1) << 32))
-                hipLaunchKernelGGL((tensor_async_staged_kernel<V, uint32_t>), grid, dim3(256), 0, s, a, S);
+                hipLaunchKernelGGL((tensor_async_staged_kernel<V, uint32_t>), grid, dim3(256), lds, s, a, S);
             else
-                hipLaunchKernelGGL((tensor_async_staged_kernel<V, int64_t>), grid, dim3(256), 0, s, a, S);
+                hipLaunchKernelGGL((tensor_async_staged_kernel<V, int64_t>), grid, dim3(256), lds, s, a, S);
             return hipGetLastError();
         }
     }
