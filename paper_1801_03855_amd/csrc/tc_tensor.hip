@@ -818,19 +818,23 @@ __global__ __launch_bounds__(256) void tensor_async_kernel(TStepArgs<float> a) {
 // in place: d = x_w - c, c = fma(alpha, d, c), x_w = fma(-alpha, d, x_w),
 // the slot kernel's operations in its order.  The exchanged workers' pieces
 // are then written back piece after piece.  The LDS is sized at launch to
-// the S rows, so that smaller K fit more workgroups per CU.  Measured on
-// MI355X, ResNet-50 group, R = K, against the slot kernel: K = 17 +19%,
-// K = 33 2.96 -> 5.08 TB/s, K = 40 and 48 +26-27%, K = 64 level; K = 24 -3%
-// and K = 32 -13%.  So it takes K between powers of two from 33, and from 17
-// while more than a quarter of the slot mapping's lanes would idle.  Two or
-// four recurrences per lane (twice or four times the rows) measured slower.
+// the S rows, S at most 64 and the rows at most 24 KiB, so that more
+// workgroups fit per CU.  Measured on MI355X, ResNet-50 group, R = K,
+// against the slot kernel: K = 17 +19%, K = 33 2.96 -> 5.09 TB/s, K = 40
+// +12% and K = 48 +12% over 64 KiB of rows (+40-45% over the slot kernel),
+// K = 56 +24%, K = 64 3.1 -> 3.8; K = 24 -3% and K = 32 -13%.  So it takes
+// every K from 33, and K = 17 to 23, where more than a quarter of the slot
+// mapping's lanes would idle.  Rows of up to 16, 32 and 64 KiB, and two or
+// four recurrences per lane, measured slower.
 #ifndef TC_TASYNC_STAGED
 #define TC_TASYNC_STAGED 1
 #endif
 #ifndef TC_TASYNC_STAGED_V
 #define TC_TASYNC_STAGED_V 1
 #endif
-constexpr int kAsyncStagedPieces = 4096;  // LDS pieces per workgroup (64 KiB)
+#ifndef TC_TASYNC_STAGED_LDS
+#define TC_TASYNC_STAGED_LDS 24576
+#endif
 template <int V, typename I>
 __global__ __launch_bounds__(256) void tensor_async_staged_kernel(TStepArgs<float> a, int S) {
     extern __shared__ f4 s_x[];  // S rows of KP pieces (sized at launch)
@@ -2251,10 +2255,11 @@ hipError_t run_tstep(const TStepArgs<T>& a, hipStream_t s) {
         }
     }
     if constexpr (OP == TOp::Async && sizeof(T) == 4 && P >= 32) {
-        if (TC_TASYNC_STAGED && a.K != P && (P >= 64 || (P - a.K) * 4 > P)) {
+        if (TC_TASYNC_STAGED && (P >= 64 || (P - a.K) * 4 > P)) {
             constexpr int V = TC_TASYNC_STAGED_V;
             const int KP = a.K | 1;
-            const int S = 64 * V < kAsyncStagedPieces / KP ? 64 * V : kAsyncStagedPieces / KP;
+            const int cap = TC_TASYNC_STAGED_LDS / 16;
+            const int S = 64 * V < cap / KP ? 64 * V : cap / KP;
             const int64_t blocks = (a.nslot + S - 1) / S;
             dim3 grid(static_cast<unsigned>(blocks < 1 ? 1 : blocks));
             const size_t lds = static_cast<size_t>(S) * KP * sizeof(f4);
